@@ -1,0 +1,112 @@
+/*
+ * nmspmm.h -- C ABI of the MI355X (gfx950) vector-wise N:M sparse matrix
+ * multiplication library (NM-SpMM, arXiv 2503.01253).
+ *
+ * Problem (Sec. II-A): C = A * B with A m x k, B k x n, C m x n, all fp32,
+ * row-major.  B is pruned with vector-wise N:M sparsity: inside every window
+ * of M consecutive k-rows, N rows are kept, and one kept set is shared by each
+ * block of V adjacent columns (the paper's vector length L).  B is stored
+ * compressed as
+ *   Bc  : w x n fp32, row-major, w = (k/M)*N            (the paper's B')
+ *   idx : w x q uint8, row-major, q = n/V                (the paper's D)
+ * where compressed row u = g*N + r (group g, r-th kept row) holds the kept
+ * row-vector of window g for each column block b, and idx[u][b] is that row's
+ * offset in [0, M) inside window g.  Offsets of one (g, b) are strictly
+ * increasing.  The product computed is Eq. 1 read as
+ *   C[i][j] = sum_{u<w} A[i][floor(u/N)*M + idx[u][floor(j/V)]] * Bc[u][j]
+ * with no M/N rescaling (a caller wanting Eq. 1's factor scales Bc).
+ *
+ * Every entry point is extern "C", returns a status code and never throws.
+ * The library holds no global state besides per-device kernel attributes
+ * and is safe to call from several host threads.
+ */
+#ifndef NMSPMM_H
+#define NMSPMM_H
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#if defined(__GNUC__)
+#define NMSPMM_API __attribute__((visibility("default")))
+#else
+#define NMSPMM_API
+#endif
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    NMSPMM_OK = 0,
+    /* null pointer where data is required, negative size, k % M != 0,
+     * n % V != 0, N < 1, N > M, M > 256, V < 1, or an idx entry that breaks
+     * the pattern rules (nmspmm_validate_idx only) */
+    NMSPMM_ERR_INVALID_ARG = 1,
+    /* a well-formed request outside what the library implements (e.g. a
+     * pointer not aligned to 4 bytes for an fp32 array, or sizes whose
+     * products overflow int64) */
+    NMSPMM_ERR_UNSUPPORTED = 2,
+    /* the HIP runtime reported an error while launching */
+    NMSPMM_ERR_HIP = 3
+} nmspmm_status_t;
+
+/* Number of fp32 elements of Bc, (k/M)*N*n, or -1 if (k, n, N, M) is invalid
+ * (Sec. II-A: w = k*N/M rows). */
+NMSPMM_API int64_t nmspmm_bc_elems(int64_t k, int64_t n, int N, int M);
+
+/* Number of bytes of idx, (k/M)*N*(n/V), or -1 if the shape is invalid
+ * (Sec. II-A: D is w x q; one uint8 per entry, enough for the log2(M) bits
+ * of Sec. III-B.1 as long as M <= 256). */
+NMSPMM_API int64_t nmspmm_idx_bytes(int64_t k, int64_t n, int N, int M, int V);
+
+/* Offline packing (Sec. II-A; the offline pre-processing of Sec. III-C.1).
+ * HOST pointers.  B_dense: k x n fp32 row-major, read only.  Bc and idx are
+ * caller-allocated with nmspmm_bc_elems / nmspmm_idx_bytes entries.
+ * For every (window g, column block b) the N row-vectors of largest squared
+ * L2 norm over the block's V columns are kept (ties to the smaller offset),
+ * their offsets written to idx in increasing order and their values copied to
+ * Bc.  On an already pruned B whose kept values are non-zero this recovers
+ * the kept set exactly.  k == 0 or n == 0 is a valid no-op.
+ * Errors: NMSPMM_ERR_INVALID_ARG for a bad shape or a null pointer with a
+ * non-empty output; nothing is written then. */
+NMSPMM_API nmspmm_status_t nmspmm_compress(const float *B_dense, int64_t k, int64_t n,
+                                int N, int M, int V, float *Bc, uint8_t *idx);
+
+/* The sparse product (Eq. 1 as read above; Sec. III describes the tiled GPU
+ * algorithm).  DEVICE pointers, all on the current HIP device.
+ *   A  : m x k fp32 row-major (read only)
+ *   Bc : w x n fp32 row-major (read only)
+ *   idx: w x q uint8 row-major (read only)
+ *   C  : m x n fp32 row-major, overwritten (must not alias the inputs)
+ * Asynchronous on `stream` (NULL = the legacy default stream): the call
+ * validates its arguments, enqueues the kernel(s) and returns; it allocates
+ * nothing and does not synchronize.  Kernel faults surface at the caller's
+ * next synchronization.  m == 0 or n == 0 returns NMSPMM_OK without a launch;
+ * k == 0 writes zeros to C.  idx contents are not validated on the device
+ * (use nmspmm_validate_idx on the host); an offset >= M is clamped to M-1
+ * so that every access stays inside A, and the result is then unspecified.
+ * Errors: NMSPMM_ERR_INVALID_ARG (bad shape, null pointer with non-empty
+ * data), NMSPMM_ERR_UNSUPPORTED (misaligned pointer), NMSPMM_ERR_HIP (the
+ * launch failed). */
+NMSPMM_API nmspmm_status_t nmspmm_run(const float *A, const float *Bc, const uint8_t *idx,
+                           float *C, int64_t m, int64_t n, int64_t k, int N,
+                           int M, int V, hipStream_t stream);
+
+/* Host check of the pattern rules (Sec. II-A): every (group, block) has N
+ * offsets, each < M, strictly increasing.  HOST pointer, O(w*q).
+ * Returns NMSPMM_OK or NMSPMM_ERR_INVALID_ARG. */
+NMSPMM_API nmspmm_status_t nmspmm_validate_idx(const uint8_t *idx, int64_t k, int64_t n,
+                                    int N, int M, int V);
+
+/* Static, never-null description of a status code. */
+NMSPMM_API const char *nmspmm_status_string(nmspmm_status_t s);
+
+/* Name of the kernel variant nmspmm_run would launch for this shape (static
+ * string, "none" when nothing is launched, "invalid" for a bad shape).  For
+ * benchmarking and profiling reports; it launches nothing. */
+NMSPMM_API const char *nmspmm_kernel_name(int64_t m, int64_t n, int64_t k, int N, int M, int V);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* NMSPMM_H */

@@ -1,0 +1,144 @@
+"""ctypes binding of libnmspmm.so: the C-ABI entry points under the same names.
+
+Argument marshalling only.  Device buffers are PyTorch tensors (torch provides
+HIP memory and streams); every step of the product runs in the library's HIP
+kernels.  There is no fallback: if the library is not built, every call
+raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+from .build import LIB_PATH
+
+NMSPMM_OK = 0
+NMSPMM_ERR_INVALID_ARG = 1
+NMSPMM_ERR_UNSUPPORTED = 2
+NMSPMM_ERR_HIP = 3
+
+EXPORTS = (
+    "nmspmm_bc_elems", "nmspmm_idx_bytes", "nmspmm_compress", "nmspmm_run",
+    "nmspmm_validate_idx", "nmspmm_status_string", "nmspmm_kernel_name",
+)
+
+
+class NmSpmmError(RuntimeError):
+    def __init__(self, fn, status, msg):
+        super().__init__(f"{fn}: {msg} (status {status})")
+        self.status = status
+
+
+_lib = None
+
+
+def lib():
+    """Load the built library.  torch is imported first so that the library
+    binds to the HIP runtime torch already loaded (same soname), keeping
+    torch's streams and allocations valid inside the library."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    import torch  # noqa: F401  (loads torch's libamdhip64 before ours)
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built: run `python -m paper_2503_01253_amd.build`")
+    L = ctypes.CDLL(LIB_PATH)
+    I64, I, P = ctypes.c_int64, ctypes.c_int, ctypes.c_void_p
+    L.nmspmm_bc_elems.argtypes = [I64, I64, I, I]
+    L.nmspmm_bc_elems.restype = I64
+    L.nmspmm_idx_bytes.argtypes = [I64, I64, I, I, I]
+    L.nmspmm_idx_bytes.restype = I64
+    L.nmspmm_compress.argtypes = [P, I64, I64, I, I, I, P, P]
+    L.nmspmm_compress.restype = I
+    L.nmspmm_run.argtypes = [P, P, P, P, I64, I64, I64, I, I, I, P]
+    L.nmspmm_run.restype = I
+    L.nmspmm_validate_idx.argtypes = [P, I64, I64, I, I, I]
+    L.nmspmm_validate_idx.restype = I
+    L.nmspmm_status_string.argtypes = [I]
+    L.nmspmm_status_string.restype = ctypes.c_char_p
+    L.nmspmm_kernel_name.argtypes = [I64, I64, I64, I, I, I]
+    L.nmspmm_kernel_name.restype = ctypes.c_char_p
+    _lib = L
+    return L
+
+
+def nmspmm_status_string(status: int) -> str:
+    return lib().nmspmm_status_string(int(status)).decode()
+
+
+def _check(fn, status):
+    if status != NMSPMM_OK:
+        raise NmSpmmError(fn, status, nmspmm_status_string(status))
+
+
+def nmspmm_bc_elems(k: int, n: int, N: int, M: int) -> int:
+    return int(lib().nmspmm_bc_elems(k, n, N, M))
+
+
+def nmspmm_idx_bytes(k: int, n: int, N: int, M: int, V: int) -> int:
+    return int(lib().nmspmm_idx_bytes(k, n, N, M, V))
+
+
+def nmspmm_kernel_name(m: int, n: int, k: int, N: int, M: int, V: int) -> str:
+    return lib().nmspmm_kernel_name(m, n, k, N, M, V).decode()
+
+
+def nmspmm_compress(B_dense: np.ndarray, N: int, M: int, V: int):
+    """Host packer: dense (pruned) B, k x n fp32 -> (Bc, idx) numpy arrays."""
+    B = np.ascontiguousarray(B_dense, dtype=np.float32)
+    if B.ndim != 2:
+        raise ValueError("B_dense must be 2-D")
+    k, n = B.shape
+    nbc = nmspmm_bc_elems(k, n, N, M)
+    nidx = nmspmm_idx_bytes(k, n, N, M, V)
+    if nbc < 0 or nidx < 0:
+        raise NmSpmmError("nmspmm_compress", NMSPMM_ERR_INVALID_ARG,
+                          f"invalid shape k={k} n={n} N={N} M={M} V={V}")
+    w = (k // M) * N
+    Bc = np.empty((w, n), dtype=np.float32)
+    idx = np.empty((w, n // V), dtype=np.uint8)
+    st = lib().nmspmm_compress(B.ctypes.data, k, n, N, M, V, Bc.ctypes.data, idx.ctypes.data)
+    _check("nmspmm_compress", st)
+    return Bc, idx
+
+
+def nmspmm_validate_idx(idx: np.ndarray, k: int, n: int, N: int, M: int, V: int) -> int:
+    """Returns the status code (0 = valid pattern)."""
+    d = np.ascontiguousarray(idx, dtype=np.uint8)
+    return int(lib().nmspmm_validate_idx(d.ctypes.data, k, n, N, M, V))
+
+
+def nmspmm_run_ptr(A: int, Bc: int, idx: int, C: int, m: int, n: int, k: int,
+                   N: int, M: int, V: int, stream: int) -> int:
+    """Raw entry point: device addresses and a hipStream_t as integers.
+    Returns the status code."""
+    return int(lib().nmspmm_run(A, Bc, idx, C, m, n, k, N, M, V, stream))
+
+
+def nmspmm_run(A, Bc, idx, C, m: int, n: int, k: int, N: int, M: int, V: int, stream=None):
+    """C = A * B_pruned on the GPU, asynchronously on ``stream`` (a
+    torch.cuda.Stream; default: torch's current stream).  A (m x k), Bc
+    (w x n), C (m x n) are contiguous fp32 CUDA tensors, idx (w x q) a
+    contiguous uint8 CUDA tensor, all on one device."""
+    import torch
+    L = lib()
+    for name, t, dt in (("A", A, torch.float32), ("Bc", Bc, torch.float32),
+                        ("idx", idx, torch.uint8), ("C", C, torch.float32)):
+        if not isinstance(t, torch.Tensor) or t.dtype != dt or not t.is_cuda or not t.is_contiguous():
+            raise TypeError(f"{name} must be a contiguous CUDA tensor of {dt}")
+        if t.device != C.device:
+            raise ValueError(f"{name} is on {t.device}, C on {C.device}")
+    w = (k // M) * N if M > 0 else 0
+    q = n // V if V > 0 else 0
+    for name, t, numel in (("A", A, m * k), ("Bc", Bc, w * n), ("idx", idx, w * q), ("C", C, m * n)):
+        if t.numel() != numel:
+            raise ValueError(f"{name} has {t.numel()} elements, expected {numel}")
+    if stream is None:
+        stream = torch.cuda.current_stream(C.device)
+    with torch.cuda.device(C.device):
+        st = L.nmspmm_run(A.data_ptr(), Bc.data_ptr(), idx.data_ptr(), C.data_ptr(),
+                          m, n, k, N, M, V, stream.cuda_stream)
+    _check("nmspmm_run", st)
+    return C

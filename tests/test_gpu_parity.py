@@ -1,0 +1,165 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle.
+
+Bar: every element finite and |C_gpu - C_ref| <= 1e-5 * sum_k |A_ik||B_kj|
+(fp32 arithmetic against an fp64 reference), and bit-exact equality on
+small-integer inputs whose partial sums are all exact in fp32.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+from nm_workloads import RUNS, make_inputs, make_run
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():  # the -m gpu suite only runs on a GPU machine
+    pytest.skip("no GPU", allow_module_level=True)
+
+import paper_2503_01253_amd as nm  # noqa: E402
+
+
+def say(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def to_dev(x):
+    return torch.from_numpy(np.ascontiguousarray(x)).cuda()
+
+
+def gpu_run(A, Bc, idx, m, n, k, N, M, V, stream=None, fill=float("nan")):
+    """Run the library on host arrays; C starts as NaN so unwritten outputs fail."""
+    dA, dBc, didx = to_dev(A), to_dev(Bc), to_dev(idx)
+    dC = torch.full((m, n), fill, dtype=torch.float32, device="cuda")
+    nm.nmspmm_run(dA, dBc, didx, dC, m, n, k, N, M, V, stream=stream)
+    torch.cuda.synchronize()
+    return dC.cpu().numpy()
+
+
+def parity(m, k, n, N, M, V, dist, seed):
+    say(f"[parity] m={m} k={k} n={n} {N}:{M} V={V} {dist} seed={seed} "
+        f"kernel={nm.nmspmm_kernel_name(m, n, k, N, M, V)}")
+    A, Bp, _ = make_inputs(m, k, n, N, M, V, seed, dist)
+    Bc, idx = nm.nmspmm_compress(Bp, N, M, V)
+    Bc_o, idx_o = oracle.compress(Bp, N, M, V)
+    assert np.array_equal(idx, idx_o) and np.array_equal(Bc, Bc_o)
+    C = gpu_run(A, Bc, idx, m, n, k, N, M, V)
+    C_ref = oracle.spmm(A, Bc_o, idx_o, m, n, k, N, M, V)
+    Bnd = oracle.bound(A, Bc_o, idx_o, m, n, k, N, M, V)
+    return C, C_ref, Bnd
+
+
+# Shapes that span several tiles and end in ragged tails, over every kernel
+# family the dispatcher has (tiled MFMA at V = 16/32/64/128/256, M = 4..32,
+# the 62.5% level 12:32, N = M; the general kernel for the rest).
+SMALL = [
+    (300, 320, 320, 16, 32, 32),
+    (300, 256, 448, 8, 32, 64),
+    (129, 128, 96, 4, 32, 16),
+    (1030, 128, 1088, 4, 32, 32),
+    (1100, 96, 1280, 16, 32, 64),
+    (65, 64, 64, 32, 32, 32),
+    (200, 192, 320, 12, 32, 32),
+    (100, 64, 128, 4, 16, 32),
+    (64, 48, 128, 4, 16, 32),
+    (70, 64, 128, 2, 8, 64),
+    (80, 64, 64, 1, 4, 16),
+    (70, 64, 256, 8, 32, 128),
+    (70, 64, 512, 8, 32, 256),
+    (1024, 64, 1024, 8, 32, 512),
+    (17, 24, 10, 3, 8, 2),
+    (33, 28, 21, 2, 7, 3),
+    (5, 64, 64, 1, 32, 32),
+    (1, 64, 64, 4, 32, 32),
+    (3, 32, 32, 4, 32, 32),
+]
+
+
+@pytest.mark.parametrize("shape", SMALL, ids=lambda s: "x".join(map(str, s)))
+@pytest.mark.parametrize("dist", ["uniform", "normal"])
+def test_parity_small(shape, dist):
+    m, k, n, N, M, V = shape
+    C, C_ref, Bnd = parity(m, k, n, N, M, V, dist, seed=m + 3 * k + 7 * n + N)
+    r = oracle.check(C, C_ref, Bnd)
+    assert r, r
+
+
+@pytest.mark.parametrize("shape", SMALL, ids=lambda s: "x".join(map(str, s)))
+def test_small_integers_exact(shape):
+    """With |a|, |b| <= 8 every partial sum is an integer below 2^24, so any
+    fp32 summation order gives the exact result: index, gather and tail bugs
+    cannot hide inside a tolerance."""
+    m, k, n, N, M, V = shape
+    C, C_ref, _ = parity(m, k, n, N, M, V, "int", seed=5 + m)
+    assert np.array_equal(C.astype(np.float64), C_ref)
+
+
+@pytest.mark.parametrize("name", list(RUNS))
+def test_parity_full_size_sampled_rows(name):
+    """Each benchmark workload at full size, in the launch the benchmark times;
+    the oracle computes a sample of rows (first, last, tile edges, random)."""
+    run = RUNS[name]
+    m, k, n, N, M, V = run.m, run.k, run.n, run.N, run.M, run.V
+    say(f"[full] {run.describe()} kernel={nm.nmspmm_kernel_name(m, n, k, N, M, V)}")
+    A, Bp, _ = make_run(run)
+    Bc, idx = nm.nmspmm_compress(Bp, N, M, V)
+    C = gpu_run(A, Bc, idx, m, n, k, N, M, V)
+    assert np.isfinite(C).all()
+    rng = np.random.default_rng(run.seed)
+    rows = {0, m - 1, min(m - 1, 127), min(m - 1, 128), min(m - 1, 255), min(m - 1, 256)}
+    rows |= set(int(x) for x in rng.integers(0, m, size=8))
+    rows = np.array(sorted(rows))
+    Bc_o, idx_o = oracle.compress(Bp, N, M, V)
+    assert np.array_equal(idx, idx_o) and np.array_equal(Bc, Bc_o)
+    As = np.ascontiguousarray(A[rows])
+    C_ref = oracle.spmm(As, Bc_o, idx_o, len(rows), n, k, N, M, V)
+    Bnd = oracle.bound(As, Bc_o, idx_o, len(rows), n, k, N, M, V)
+    r = oracle.check(C[rows], C_ref, Bnd)
+    say(f"[full] {name}: {r}")
+    assert r, r
+
+
+def test_k_zero_writes_zeros_and_m_zero_is_noop():
+    C = gpu_run(np.zeros((40, 0), np.float32), np.zeros((0, 64), np.float32),
+                np.zeros((0, 2), np.uint8), 40, 64, 0, 4, 32, 32)
+    assert np.all(C == 0)
+    dC = torch.full((0, 64), 1.0, device="cuda")
+    nm.nmspmm_run(torch.zeros((0, 64), device="cuda"), torch.zeros((8, 64), device="cuda"),
+                  torch.zeros((8, 2), dtype=torch.uint8, device="cuda"), dC, 0, 64, 64, 4, 32, 32)
+    torch.cuda.synchronize()
+
+
+def test_deterministic_and_stream_ordered():
+    m, k, n, N, M, V = 1030, 256, 1088, 8, 32, 32
+    A, Bp, _ = make_inputs(m, k, n, N, M, V, 99)
+    Bc, idx = nm.nmspmm_compress(Bp, N, M, V)
+    C1 = gpu_run(A, Bc, idx, m, n, k, N, M, V)
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        C2 = gpu_run(A, Bc, idx, m, n, k, N, M, V, stream=s)
+    assert C1.tobytes() == C2.tobytes()
+
+
+@pytest.mark.parametrize("scale", [2.0, 4.0, 8.0])
+def test_power_of_two_scaling_is_exact(scale):
+    """Eq. 1's M/N factor, applied by the caller to Bc, scales C exactly."""
+    m, k, n, N, M, V = 300, 256, 320, 32 // int(scale), 32, 32
+    A, Bp, _ = make_inputs(m, k, n, N, M, V, 17)
+    Bc, idx = nm.nmspmm_compress(Bp, N, M, V)
+    C = gpu_run(A, Bc, idx, m, n, k, N, M, V)
+    Cs = gpu_run(A, (Bc * np.float32(scale)).astype(np.float32), idx, m, n, k, N, M, V)
+    assert np.array_equal(Cs, C * np.float32(scale))
+
+
+def test_out_of_range_offsets_stay_in_bounds():
+    """An offset >= M is outside the contract; the kernel clamps it, so the
+    call completes and writes finite values."""
+    m, k, n, N, M, V = 300, 128, 320, 8, 32, 32
+    A, Bp, _ = make_inputs(m, k, n, N, M, V, 3)
+    Bc, idx = nm.nmspmm_compress(Bp, N, M, V)
+    idx = idx.copy()
+    idx[::3, ::2] = 255
+    C = gpu_run(A, Bc, idx, m, n, k, N, M, V)
+    assert np.isfinite(C).all()
