@@ -1,0 +1,265 @@
+"""Benchmark of the vector-wise N:M SpMM hot path on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload R2]
+                    [--no-sweep] [--no-cpu-baseline]
+
+A step is one call of nmspmm_run (the whole device path: gathered staging,
+MFMA contraction, store) on the headline workload, m = n = k = 4096 fp32 at
+16:32 (50 %) with V = 32.  Inputs are generated on the host, packed with
+nmspmm_compress (offline, untimed) and resident in HBM before timing; the
+timed launches rotate over enough copies of (A, Bc, idx, C) that no launch
+finds its operands in L2 or the 256 MB Infinity Cache.
+
+Prints ONE JSON line: the headline value (effective TFLOPS on useful flops
+2 m n k N/M), the roofline of the kernel (per-launch HIP-event durations on
+the launch stream), the CPU oracle timed on the host, a sweep over the other
+workloads (75 / 87.5 % sparsity, the MLP shape, skinny decode shapes) and a
+dense fp32 torch.matmul comparison.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import statistics
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+from nm_workloads import RUNS, make_run  # noqa: E402
+
+PEAK_FP32_TFLOPS = 157.3     # MI355X dense fp32 (vector = matrix), AMD spec
+PEAK_HBM_GBS = 8000.0        # MI355X HBM3E, AMD spec
+CACHE_BYTES = 288 << 20      # 256 MB Infinity Cache + 8 x 4 MB L2
+
+# HBM traffic of the headline kernel from rocprofv3 --pmc FETCH_SIZE and
+# WRITE_SIZE (KiB per dispatch), each scaled by the factor the same counter
+# reads for a copy kernel of known size.  Valid only for the kernel source
+# hash it was taken on; null otherwise.
+TRAFFIC = {}
+
+
+def kernel_source_sha():
+    p = os.path.join(ROOT, "paper_2503_01253_amd", "csrc", "nmspmm_kernels.hip")
+    return hashlib.sha256(open(p, "rb").read()).hexdigest()[:16]
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+class Workload:
+    """Device-resident copies of one run's operands, rotated across launches."""
+
+    def __init__(self, run, torch, nm, min_copies=1, with_dense=False):
+        self.run = run
+        self.torch = torch
+        self.nm = nm
+        A, Bp, _ = make_run(run)
+        Bc, idx = nm.nmspmm_compress(Bp, run.N, run.M, run.V)
+        per_copy = A.nbytes + Bc.nbytes + idx.nbytes + 4 * run.m * run.n
+        self.copies = max(min_copies, int(np.ceil(2 * CACHE_BYTES / per_copy)))
+        dev = torch.device("cuda")
+        tA, tBc, tidx = (torch.from_numpy(x).to(dev) for x in (A, Bc, idx))
+        self.sets = []
+        for c in range(self.copies):
+            self.sets.append((tA if c == 0 else tA.clone(), tBc if c == 0 else tBc.clone(),
+                              tidx if c == 0 else tidx.clone(),
+                              torch.empty((run.m, run.n), dtype=torch.float32, device=dev)))
+        self.ptrs = [(a.data_ptr(), b.data_ptr(), i.data_ptr(), c.data_ptr()) for a, b, i, c in self.sets]
+        self.dense = None
+        if with_dense:
+            tB = torch.from_numpy(Bp).to(dev)
+            self.dense = [(s[0], tB if c == 0 else tB.clone(), torch.empty_like(s[3]))
+                          for c, s in enumerate(self.sets)]
+        self.host_A, self.host_Bp = A, Bp
+
+    def launch(self, i, stream_handle):
+        r = self.run
+        a, b, x, c = self.ptrs[i % self.copies]
+        st = self.nm.nmspmm_run_ptr(a, b, x, c, r.m, r.n, r.k, r.N, r.M, r.V, stream_handle)
+        if st != 0:
+            raise RuntimeError(f"nmspmm_run failed: {self.nm.nmspmm_status_string(st)}")
+
+    def launch_dense(self, i):
+        a, b, c = self.dense[i % self.copies]
+        self.torch.matmul(a, b, out=c)
+
+    def free(self):
+        self.sets = None
+        self.dense = None
+
+
+def time_launches(torch, fn, steps, warmup):
+    """Warm up, then time `steps` launches: total wall (events around the
+    whole batch) and per-launch durations (an event pair around each launch,
+    on the stream the kernel runs on)."""
+    stream = torch.cuda.current_stream()
+    for i in range(warmup):
+        fn(i)
+    torch.cuda.synchronize()
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
+    ends = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0.record(stream)
+    for i in range(steps):
+        starts[i].record(stream)
+        fn(warmup + i)
+        ends[i].record(stream)
+    t1.record(stream)
+    torch.cuda.synchronize()
+    per = [s.elapsed_time(e) for s, e in zip(starts, ends)]
+    return t0.elapsed_time(t1), per
+
+
+def cpu_baseline(run, A, Bp, target_s):
+    """The fp64 CPU oracle on the same workload, timed on the host cores."""
+    import oracle
+    Bc, idx = oracle.compress(Bp, run.N, run.M, run.V)
+    threads = oracle.max_threads()
+    # calibrate on a few rows, then pick a row sample worth about target_s
+    rows = min(run.m, 16)
+    t = time.perf_counter()
+    oracle.spmm(A[:rows], Bc, idx, rows, run.n, run.k, run.N, run.M, run.V)
+    per_row = max(time.perf_counter() - t, 1e-6) / rows
+    rows = int(min(run.m, max(1, target_s / per_row)))
+    reps = max(1, int(target_s / (per_row * rows)))
+    As = np.ascontiguousarray(A[:rows])
+    times = []
+    for _ in range(reps):
+        t = time.perf_counter()
+        oracle.spmm(As, Bc, idx, rows, run.n, run.k, run.N, run.M, run.V)
+        times.append(time.perf_counter() - t)
+    dt = statistics.median(times)
+    flops = 2.0 * rows * run.n * run.w
+    return {
+        "value": flops / dt / 1e12, "unit": "TFLOPS", "cores": threads, "kind": "oracle",
+        "sample": (f"{run.name}: {rows} of {run.m} rows of A (full k, n), fp64 oracle, "
+                   f"median of {reps} run(s), {dt:.2f} s each"),
+    }
+
+
+def measure(torch, nm, run, steps, warmup, with_dense):
+    w = Workload(run, torch, nm, with_dense=with_dense)
+    handle = torch.cuda.current_stream().cuda_stream
+    total_ms, per = time_launches(torch, lambda i: w.launch(i, handle), steps, warmup)
+    res = {
+        "workload": run.name, "m": run.m, "n": run.n, "k": run.k, "N": run.N, "M": run.M,
+        "V": run.V, "kernel": nm.nmspmm_kernel_name(run.m, run.n, run.k, run.N, run.M, run.V),
+        "copies": w.copies, "ms_per_step": total_ms / steps,
+        "kernel_ms_mean": statistics.fmean(per), "kernel_ms_median": statistics.median(per),
+    }
+    res["eff_tflops"] = run.useful_flops / (res["kernel_ms_median"] * 1e-3) / 1e12
+    res["hbm_gbs_alg"] = run.alg_bytes / (res["kernel_ms_median"] * 1e-3) / 1e9
+    ai = run.useful_flops / run.alg_bytes
+    roof = min(PEAK_FP32_TFLOPS, ai * PEAK_HBM_GBS / 1e3)
+    res["roof_tflops"] = roof
+    res["roof_frac"] = res["eff_tflops"] / roof
+    res["bound"] = "hbm" if ai * PEAK_HBM_GBS / 1e3 < PEAK_FP32_TFLOPS else "fp32"
+    if with_dense:
+        d_total, d_per = time_launches(torch, w.launch_dense, max(10, steps // 4), 3)
+        d_ms = statistics.median(d_per)
+        res["dense_matmul_ms"] = d_ms
+        res["speedup_vs_dense"] = d_ms / res["kernel_ms_median"]
+        res["ideal_speedup"] = run.M / run.N
+    w.free()
+    return res, w
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="R2", choices=sorted(RUNS))
+    ap.add_argument("--no-sweep", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU: the N:M SpMM path runs on a single MI355X "
+              f"and has no multi-GPU mode (asked for --gpus {args.gpus}).", file=sys.stderr)
+        sys.exit(2)
+    if int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py is single-process; WORLD_SIZE > 1 is not supported.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2503_01253_amd as nm
+    torch.backends.cuda.matmul.allow_tf32 = False
+    torch.set_float32_matmul_precision("highest")
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+
+    run = RUNS[args.workload]
+    log(f"[bench] headline {run.describe()} steps={args.steps} warmup={args.warmup}")
+    head, w = measure(torch, nm, run, args.steps, args.warmup, with_dense=True)
+    log(f"[bench] {json.dumps(head)}")
+
+    achieved = run.useful_flops / (head["kernel_ms_mean"] * 1e-3) / 1e12
+    sha = kernel_source_sha()
+    tr = TRAFFIC.get((run.name, sha))
+    roofline = {
+        "bound": "mfma", "achieved": achieved, "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s",
+        "frac": achieved / PEAK_FP32_TFLOPS, "traffic": tr,
+        "kernel": head["kernel"], "kernel_ms_mean": head["kernel_ms_mean"],
+        "flops_per_launch": run.useful_flops, "alg_bytes_per_launch": run.alg_bytes,
+        "kernel_src_sha": sha,
+    }
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("[bench] cpu baseline (oracle)")
+        cpu = cpu_baseline(run, w.host_A, w.host_Bp, args.cpu_seconds)
+        log(f"[bench] cpu {json.dumps(cpu)}")
+
+    sweep = []
+    if not args.no_sweep:
+        for name in ("R1", "R3a", "R3b", "R3c", "R3d", "R4", "R5a", "R5b", "R5c"):
+            if name == run.name:
+                continue
+            r = RUNS[name]
+            steps = 200 if r.m <= 256 else 30
+            res, _ = measure(torch, nm, r, steps, 5, with_dense=True)
+            log(f"[bench] sweep {json.dumps(res)}")
+            sweep.append({k: (round(v, 5) if isinstance(v, float) else v) for k, v in res.items()})
+            torch.cuda.empty_cache()
+
+    ms = head["ms_per_step"]
+    line = {
+        "metric": "effective TFLOPS (2*m*n*k*N/M)",
+        "value": run.useful_flops / (ms * 1e-3) / 1e12,
+        "unit": "TFLOPS",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f32", "data": "synthetic",
+        "config": {
+            "workload": (f"m=n=k=4096 fp32, A,B ~ U[-1,1], vector-wise {run.N}:{run.M} "
+                         f"({100 * (1 - run.N / run.M):.1f}% sparse), V={run.V}")
+            if run.name == "R2" else run.describe(),
+            "m": run.m, "n": run.n, "k": run.k, "N": run.N, "M": run.M, "V": run.V,
+            "seed": run.seed, "parallelism": "single GPU", "cold_cache_copies": head["copies"],
+        },
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "dense_fp32_matmul": {"ms": head["dense_matmul_ms"], "speedup": head["speedup_vs_dense"],
+                              "ideal_speedup": head["ideal_speedup"]},
+        "paper_context": {"hardware": "NVIDIA A100 80GB PCIe (clock locked, 14.7 TFLOPS fp32 peak)",
+                          "workload": "m=n=k=4096, vector length not stated",
+                          "pct_of_fp32_peak_50_62.5_75_87.5": [96, 93, 95, 88]},
+        "sweep": sweep,
+        "device": torch.cuda.get_device_name(0),
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()
