@@ -101,9 +101,11 @@ NMSPMM_API nmspmm_status_t nmspmm_validate_idx(const uint8_t *idx, int64_t k, in
 /* Static, never-null description of a status code. */
 NMSPMM_API const char *nmspmm_status_string(nmspmm_status_t s);
 
-/* Name of the kernel variant nmspmm_run would launch for this shape (static
- * string, "none" when nothing is launched, "invalid" for a bad shape).  For
- * benchmarking and profiling reports; it launches nothing. */
+/* Name of the kernel variant nmspmm_run would launch for this shape, assuming
+ * buffers aligned as the allocator returns them: "none" when nothing is
+ * launched, "invalid" for a bad shape.  The string stays valid until the next
+ * call from the same thread.  For benchmark and profile reports; it launches
+ * nothing. */
 NMSPMM_API const char *nmspmm_kernel_name(int64_t m, int64_t n, int64_t k, int N, int M, int V);
 
 #ifdef __cplusplus

@@ -121,7 +121,7 @@ def test_status_strings():
 
 
 def test_kernel_selection():
-    assert nm.nmspmm_kernel_name(4096, 4096, 4096, 16, 32, 32).startswith("nm_mfma_kernel")
+    assert nm.nmspmm_kernel_name(4096, 4096, 4096, 16, 32, 32).startswith("nm_tiled_kernel<")
     assert nm.nmspmm_kernel_name(5, 12, 8, 1, 4, 1) == "nm_general_kernel"
     assert nm.nmspmm_kernel_name(0, 64, 64, 4, 32, 32) == "none"
     assert nm.nmspmm_kernel_name(8, 64, 65, 4, 32, 32) == "invalid"
