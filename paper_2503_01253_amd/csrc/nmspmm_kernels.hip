@@ -69,8 +69,8 @@ __global__ __launch_bounds__(256) void nm_zero_kernel(float *__restrict__ C, int
 struct TileInfo {
     const char *name;
     int BM, BN;
-    hipError_t (*launch)(int, int, const TiledArgs &, hipStream_t);
-    bool (*fits)(int, int);
+    hipError_t (*launch)(int, int, int, const TiledArgs &, hipStream_t);
+    bool (*fits)(int, int, int);
 };
 
 const TileInfo TILES[] = {
@@ -79,6 +79,8 @@ const TileInfo TILES[] = {
     {"128x128", 128, 128, launch_tiled_128x128, tiled_fits_128x128},
     {"64x512", 64, 512, launch_tiled_64x512, tiled_fits_64x512},
     {"16x512", 16, 512, launch_tiled_16x512, tiled_fits_16x512},
+    {"256x256w16", 256, 256, launch_tiled_256x256w16, tiled_fits_256x256w16},
+    {"128x512w16", 128, 512, launch_tiled_128x512w16, tiled_fits_128x512w16},
 };
 constexpr int NTILES = sizeof(TILES) / sizeof(TILES[0]);
 
@@ -94,38 +96,44 @@ enum class Kind { None, General, Tiled };
 struct Plan {
     Kind kind = Kind::None;
     const TileInfo *tile = nullptr;
-    int BV = 0, NQ = 0, RS = 0, stages = 0, splits = 1, tiles_m = 0, tiles_n = 0;
+    int BV = 0, KA = 0, NQ = 0, RS = 0, stages = 0, splits = 1, tiles_m = 0, tiles_n = 0;
 };
 
 bool aligned(const void *p, int bytes) { return (reinterpret_cast<uintptr_t>(p) % bytes) == 0; }
 
-int round_nq(int nq) { return nq <= 4 ? nq : 8; }
+// Quads per stage actually instantiated for a stage depth of KA columns of A
+// (the smallest that holds RS compressed rows), 0 if none.
+int stage_nq(int KA, int RS)
+{
+    static const int shapes[][2] = {{32, 1}, {32, 2}, {32, 3}, {32, 4}, {32, 8},
+                                    {64, 2}, {64, 4}, {128, 1}, {128, 2}, {128, 4}};
+    int best = 0;
+    for (const auto &sh : shapes)
+        if (sh[0] == KA && 4 * sh[1] >= RS && (best == 0 || sh[1] < best)) best = sh[1];
+    return best;
+}
 
-bool tile_ok(const TileInfo &t, int BV, int NQ, int64_t k, int V)
+bool tile_ok(const TileInfo &t, int BV, int KA, int NQ, int64_t k, int V)
 {
     if (!(t.BN % V == 0 || V % t.BN == 0)) return false;
-    if (!t.fits(BV, NQ)) return false;
+    if (!t.fits(BV, KA, NQ)) return false;
     return (int64_t)t.BM * k * 4 < (int64_t(1) << 31);
 }
 
-// Tile-shape preference by problem size (measured on MI355X; see the design
-// notes).  Small m uses short, wide tiles and split-k to fill the 256 CUs.
-int preferences(int64_t m, int64_t n, int NQ, const TileInfo **out)
+// Tile-shape preference by problem size, from sweeps on MI355X: for large
+// m the 128 x 512 tile with sixteen 64 x 64 wave tiles is fastest at every
+// sparsity level measured (50 / 75 / 87.5 %), for m <= 128 rows the 16-row
+// tile with split-k, which keeps enough workgroups in flight to stream Bc.
+int preferences(int64_t m, int64_t n, const TileInfo **out)
 {
     int c = 0;
     auto add = [&](const char *name) { out[c++] = tile_by_name(name); };
-    if (m <= 16) {
+    if (m <= 128) {
         add("16x512"); add("64x512"); add("128x128");
-    } else if (m <= 64) {
-        add("64x512"); add("128x128");
-    } else if (m <= 128) {
-        add("128x512"); add("128x128");
     } else if (m < 1024 || n < 1024) {
-        add("128x128"); add("128x512"); add("256x256");
-    } else if (NQ <= 2) {
-        add("128x512"); add("256x256"); add("128x128");
+        add("128x128"); add("128x512w16"); add("256x256w16");
     } else {
-        add("256x256"); add("128x512"); add("128x128");
+        add("128x512w16"); add("256x256w16"); add("128x512"); add("256x256"); add("128x128");
     }
     return c;
 }
@@ -136,33 +144,58 @@ Plan make_plan(const float *A, const float *Bc, const float *C, int64_t m, int64
     Plan p;
     if (m == 0 || n == 0) return p;
     p.kind = Kind::General;
-    if (32 % M != 0 || k % 4 != 0 || V % 16 != 0) return p;
+    if (k % 4 != 0 || V % 16 != 0 || 128 % M != 0) return p;
     const int BV = V % 64 == 0 ? 4 : (V % 32 == 0 ? 2 : 1);
     if (!aligned(A, 16) || !aligned(Bc, 16) || !aligned(C, 4 * BV)) return p;
-    const int RS = (32 / M) * N;
-    const int NQ = round_nq((RS + 3) / 4);
     // per-stage Bc buffer offsets reach (padded rows) x n x 4 bytes < 32 x n x 4
     if ((int64_t)32 * n * 4 >= (int64_t(1) << 31)) return p;
 
+    // Stage depth: the smallest KA (a multiple of 32 and of M) whose stage
+    // holds at least 16 compressed rows, so every stage carries enough MFMA
+    // work to cover its fixed cost; deeper ones are tried if it does not fit.
+    int ka_order[3], nka = 0;
+    for (int KA : {32, 64, 128})
+        if (KA % M == 0 && (KA / M) * N >= 16) ka_order[nka++] = KA;
+    for (int KA : {128, 64, 32})
+        if (KA % M == 0 && (KA / M) * N < 16) ka_order[nka++] = KA;
+    if (const char *force = std::getenv("NMSPMM_KA")) {  // tuning sweeps only
+        const int ka = std::atoi(force);
+        if (ka == 32 || ka == 64 || ka == 128) { ka_order[0] = ka; nka = 1; }
+    }
+
     const TileInfo *cand[8];
-    int nc = preferences(m, n, NQ, cand);
+    int nc = preferences(m, n, cand);
     if (const char *force = std::getenv("NMSPMM_TILE")) {  // tuning sweeps only
         const TileInfo *t = tile_by_name(force);
         if (t) { cand[0] = t; nc = 1; }
     }
+    // first tile shape (in preference order) that some stage depth fits
     const TileInfo *tile = nullptr;
-    for (int i = 0; i < nc && !tile; ++i)
-        if (cand[i] && tile_ok(*cand[i], BV, NQ, k, V)) tile = cand[i];
+    int KA = 0, NQ = 0;
+    for (int j = 0; j < nc && !tile; ++j) {
+        if (!cand[j]) continue;
+        for (int i = 0; i < nka && !tile; ++i) {
+            const int nq = stage_nq(ka_order[i], (ka_order[i] / M) * N);
+            if (nq != 0 && tile_ok(*cand[j], BV, ka_order[i], nq, k, V)) {
+                tile = cand[j];
+                KA = ka_order[i];
+                NQ = nq;
+            }
+        }
+    }
     if (!tile) return p;
 
     const int64_t tiles_m = (m + tile->BM - 1) / tile->BM, tiles_n = (n + tile->BN - 1) / tile->BN;
-    const int64_t groups = k / M, gps = 32 / M;
+    const int64_t groups = k / M, gps = KA / M;
     const int64_t stages = (groups + gps - 1) / gps;
     if (tiles_m * tiles_n > (1 << 24) || stages > INT32_MAX) return p;
     const int64_t ntiles = tiles_m * tiles_n;
-    // split k until the grid has about one workgroup per CU
+    // split k until the grid has about one workgroup per CU (half that for
+    // the thinnest products, where fewer, longer k slices stream better)
+    const int64_t target = m <= 16 ? 128 : 256;
     int64_t splits = 1;
-    if (ntiles < 256 && stages > 1) splits = std::min<int64_t>({(256 + ntiles - 1) / ntiles, stages, 32});
+    if (ntiles < target && stages > 1)
+        splits = std::min<int64_t>({(target + ntiles - 1) / ntiles, stages, 32});
     if (const char *force = std::getenv("NMSPMM_SPLITS")) {  // tuning sweeps only
         const int64_t s = std::atoll(force);
         if (s >= 1) splits = std::min<int64_t>(s, std::max<int64_t>(stages, 1));
@@ -170,8 +203,9 @@ Plan make_plan(const float *A, const float *Bc, const float *C, int64_t m, int64
     p.kind = Kind::Tiled;
     p.tile = tile;
     p.BV = BV;
+    p.KA = KA;
     p.NQ = NQ;
-    p.RS = RS;
+    p.RS = (KA / M) * N;
     p.stages = (int)stages;
     p.splits = (int)splits;
     p.tiles_m = (int)tiles_m;
@@ -217,7 +251,7 @@ hipError_t launch_plan(const Plan &p, const float *A, const float *Bc, const uin
     a.splits = p.splits;
     a.tiles_m = p.tiles_m;
     a.tiles_n = p.tiles_n;
-    return p.tile->launch(p.BV, p.NQ, a, stream);
+    return p.tile->launch(p.BV, p.KA, p.NQ, a, stream);
 }
 
 }  // namespace
@@ -237,8 +271,8 @@ extern "C" const char *nmspmm_kernel_name(int64_t m, int64_t n, int64_t k, int N
     case Kind::Tiled: break;
     }
     thread_local char buf[96];
-    std::snprintf(buf, sizeof buf, "nm_tiled_kernel<%s,bv%d,nq%d>%s%d", p.tile->name, p.BV, p.NQ,
-                  p.splits > 1 ? "+zero,split" : ",split", p.splits);
+    std::snprintf(buf, sizeof buf, "nm_tiled_kernel<%s,bv%d,ka%d,nq%d>%s%d", p.tile->name, p.BV,
+                  p.KA, p.NQ, p.splits > 1 ? "+zero,split" : ",split", p.splits);
     return buf;
 }
 

@@ -9,14 +9,16 @@ namespace nmspmm {
 struct TiledArgs;
 
 #define NMSPMM_DECLARE_TILE(name)                                                         \
-    hipError_t launch_tiled_##name(int BV, int NQ, const TiledArgs &a, hipStream_t stream); \
-    bool tiled_fits_##name(int BV, int NQ);
+    hipError_t launch_tiled_##name(int BV, int KA, int NQ, const TiledArgs &a, hipStream_t stream); \
+    bool tiled_fits_##name(int BV, int KA, int NQ);
 
 NMSPMM_DECLARE_TILE(256x256)
 NMSPMM_DECLARE_TILE(128x512)
 NMSPMM_DECLARE_TILE(128x128)
 NMSPMM_DECLARE_TILE(64x512)
 NMSPMM_DECLARE_TILE(16x512)
+NMSPMM_DECLARE_TILE(256x256w16)
+NMSPMM_DECLARE_TILE(128x512w16)
 
 #undef NMSPMM_DECLARE_TILE
 
