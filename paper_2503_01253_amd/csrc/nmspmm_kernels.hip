@@ -1,6 +1,7 @@
 // Device half of the C ABI: the general kernel, the split-k zero fill and
 // the dispatch behind nmspmm_run (the tiled MFMA kernel lives in
-// nmspmm_tiled.h, instantiated per tile shape in nmspmm_tiled_*.hip).
+// nmspmm_tiled.h, instantiated per tile shape in nmspmm_tiled_*.hip; the
+// streaming kernel for short products in nmspmm_skinny.hip).
 //
 // Notation as in the public header: A m x k, Bc w x n, idx w x q (uint8),
 // C m x n; w = (k/M)*N, q = n/V; compressed row u belongs to window u/N.
@@ -14,6 +15,7 @@
 
 #include "nmspmm.h"
 #include "nmspmm_internal.h"
+#include "nmspmm_skinny.h"
 #include "nmspmm_tiled.h"
 #include "nmspmm_tiles.h"
 
@@ -68,19 +70,21 @@ __global__ __launch_bounds__(256) void nm_zero_kernel(float *__restrict__ C, int
 // ---------------------------------------------------------------------------
 struct TileInfo {
     const char *name;
-    int BM, BN;
+    int BM, BN, MI, waves;
     hipError_t (*launch)(int, int, int, const TiledArgs &, hipStream_t);
     bool (*fits)(int, int, int);
 };
 
 const TileInfo TILES[] = {
-    {"256x256", 256, 256, launch_tiled_256x256, tiled_fits_256x256},
-    {"128x512", 128, 512, launch_tiled_128x512, tiled_fits_128x512},
-    {"128x128", 128, 128, launch_tiled_128x128, tiled_fits_128x128},
-    {"64x512", 64, 512, launch_tiled_64x512, tiled_fits_64x512},
-    {"16x512", 16, 512, launch_tiled_16x512, tiled_fits_16x512},
-    {"256x256w16", 256, 256, launch_tiled_256x256w16, tiled_fits_256x256w16},
-    {"128x512w16", 128, 512, launch_tiled_128x512w16, tiled_fits_128x512w16},
+    {"256x256", 256, 256, 16, 8, launch_tiled_256x256, tiled_fits_256x256},
+    {"128x512", 128, 512, 16, 8, launch_tiled_128x512, tiled_fits_128x512},
+    {"128x128", 128, 128, 16, 4, launch_tiled_128x128, tiled_fits_128x128},
+    {"64x512", 64, 512, 16, 8, launch_tiled_64x512, tiled_fits_64x512},
+    {"16x512", 16, 512, 16, 8, launch_tiled_16x512, tiled_fits_16x512},
+    {"256x256m32", 256, 256, 32, 8, launch_tiled_256x256m32, tiled_fits_256x256m32},
+    {"128x512m32", 128, 512, 32, 8, launch_tiled_128x512m32, tiled_fits_128x512m32},
+    {"128x128m32", 128, 128, 32, 2, launch_tiled_128x128m32, tiled_fits_128x128m32},
+    {"64x512m32", 64, 512, 32, 8, launch_tiled_64x512m32, tiled_fits_64x512m32},
 };
 constexpr int NTILES = sizeof(TILES) / sizeof(TILES[0]);
 
@@ -91,12 +95,13 @@ const TileInfo *tile_by_name(const char *name)
     return nullptr;
 }
 
-enum class Kind { None, General, Tiled };
+enum class Kind { None, General, Tiled, Skinny };
 
 struct Plan {
     Kind kind = Kind::None;
     const TileInfo *tile = nullptr;
     int BV = 0, KA = 0, NQ = 0, RS = 0, stages = 0, splits = 1, tiles_m = 0, tiles_n = 0;
+    int QPW = 0;
 };
 
 bool aligned(const void *p, int bytes) { return (reinterpret_cast<uintptr_t>(p) % bytes) == 0; }
@@ -113,6 +118,15 @@ int stage_nq(int KA, int RS)
     return best;
 }
 
+// Column-group width of one MFMA read of B (columns per lane) for an MFMA of
+// MI columns: the widest of 4 / 2 / 1 whose group MI*BV divides V; 0 if none.
+int bv_for(int MI, int V)
+{
+    for (int bv : {4, 2, 1})
+        if (V % (MI * bv) == 0) return bv;
+    return 0;
+}
+
 bool tile_ok(const TileInfo &t, int BV, int KA, int NQ, int64_t k, int V)
 {
     if (!(t.BN % V == 0 || V % t.BN == 0)) return false;
@@ -120,22 +134,88 @@ bool tile_ok(const TileInfo &t, int BV, int KA, int NQ, int64_t k, int V)
     return (int64_t)t.BM * k * 4 < (int64_t(1) << 31);
 }
 
-// Tile-shape preference by problem size, from sweeps on MI355X: for large
-// m the 128 x 512 tile with sixteen 64 x 64 wave tiles is fastest at every
-// sparsity level measured (50 / 75 / 87.5 %), for m <= 128 rows the 16-row
-// tile with split-k, which keeps enough workgroups in flight to stream Bc.
-int preferences(int64_t m, int64_t n, const TileInfo **out)
+// Fraction of the workgroup slots a tile grid keeps busy over its waves of
+// workgroups (the last wave is usually partial), with slots = CUs x
+// workgroups per CU.
+double occupancy_of_grid(const TileInfo &t, int64_t m, int64_t n)
+{
+    const int64_t tiles = ((m + t.BM - 1) / t.BM) * ((n + t.BN - 1) / t.BN);
+    const int64_t slots = 256 * (t.waves <= 4 ? 2 : 1);
+    const int64_t rounds = (tiles + slots - 1) / slots;
+    return (double)tiles / (double)(rounds * slots);
+}
+
+// Tile-shape preference by problem size, from sweeps on MI355X:
+//  * m <= 128: 16- and 64-row tiles with split-k, which keep enough
+//    workgroups in flight to stream Bc;
+//  * m or n below 1024: the 128 x 128 tile (enough tiles to fill the chip);
+//  * otherwise the 256 x 256 tile for dense-ish levels (N/M >= 1/2) and the
+//    128 x 512 tile with 32 x 32 MFMAs for the sparser ones, unless its grid
+//    would leave more than a quarter of the chip idle in the last wave, where
+//    the 128 x 128 tile quantises better.
+int preferences(int64_t m, int64_t n, int N, int M, const TileInfo **out)
 {
     int c = 0;
     auto add = [&](const char *name) { out[c++] = tile_by_name(name); };
     if (m <= 128) {
         add("16x512"); add("64x512"); add("128x128");
-    } else if (m < 1024 || n < 1024) {
-        add("128x128"); add("128x512w16"); add("256x256w16");
-    } else {
-        add("128x512w16"); add("256x256w16"); add("128x512"); add("256x256"); add("128x128");
+        return c;
     }
+    if (m < 1024 || n < 1024) {
+        add("128x128"); add("128x512"); add("256x256");
+        return c;
+    }
+    const char *big = 2 * N >= M ? "256x256" : "128x512m32";
+    const TileInfo *bt = tile_by_name(big), *st = tile_by_name("128x128");
+    if (occupancy_of_grid(*bt, m, n) < 0.75 && occupancy_of_grid(*st, m, n) > occupancy_of_grid(*bt, m, n))
+        add("128x128");
+    add(big);
+    if (2 * N >= M) { add("128x512m32"); } else { add("256x256"); }
+    add("128x512"); add("128x128");
     return c;
+}
+
+// Rows of C up to which the streaming kernel is used (it re-reads Bc once
+// per 16 rows, the tiled kernel once per 128 or more).
+constexpr int64_t SKINNY_MAX_M = 16;
+
+int env_int(const char *name, int fallback)  // tuning sweeps only
+{
+    const char *v = std::getenv(name);
+    return v ? std::atoi(v) : fallback;
+}
+
+// Streaming kernel for short products: every Bc value is loaded once per
+// 16 rows of C straight into MFMA operands; k is split across workgroups
+// until the grid has about one workgroup per CU.
+bool plan_skinny(const float *A, const float *Bc, const float *C, int64_t m, int64_t n, int64_t k,
+                 int N, int M, int V, Plan &p)
+{
+    if (V % 16 != 0 || !aligned(A, 4) || !aligned(Bc, 16) || !aligned(C, 16)) return false;
+    // buffer offsets: 16 rows of A and 4 rows of Bc per resource
+    if ((int64_t)skinny_rows() * k * 4 >= (int64_t(1) << 31)) return false;
+    if ((int64_t)4 * n * 4 >= (int64_t(1) << 31)) return false;
+    const int bv = bv_for(16, V);
+    const int64_t tiles_m = (m + skinny_rows() - 1) / skinny_rows();
+    const int64_t tiles_n = (n + skinny_cols() - 1) / skinny_cols();
+    if (tiles_m * tiles_n > (1 << 24)) return false;
+    const int64_t w = (k / M) * N, quads = (w + 3) / 4, ntiles = tiles_m * tiles_n;
+    // at least one quad per wave and split
+    int64_t splits = std::max<int64_t>(1, std::min<int64_t>((256 + ntiles - 1) / ntiles, quads / 8));
+    splits = std::min<int64_t>(splits, 64);
+    const int fs = env_int("NMSPMM_SPLITS", 0);
+    if (fs >= 1) splits = std::min<int64_t>(fs, std::max<int64_t>(quads, 1));
+    int qpw = bv == 4 ? 4 : 2;
+    const int fq = env_int("NMSPMM_QPW", 0);
+    if (skinny_has(bv, fq)) qpw = fq;
+    if (ntiles * splits > INT32_MAX) return false;
+    p.kind = Kind::Skinny;
+    p.BV = bv;
+    p.QPW = qpw;
+    p.splits = (int)splits;
+    p.tiles_m = (int)tiles_m;
+    p.tiles_n = (int)tiles_n;
+    return true;
 }
 
 Plan make_plan(const float *A, const float *Bc, const float *C, int64_t m, int64_t n, int64_t k,
@@ -143,43 +223,57 @@ Plan make_plan(const float *A, const float *Bc, const float *C, int64_t m, int64
 {
     Plan p;
     if (m == 0 || n == 0) return p;
+    const char *force_tile = std::getenv("NMSPMM_TILE");  // tuning sweeps only
+    const bool want_skinny = force_tile ? std::strcmp(force_tile, "skinny") == 0 : m <= SKINNY_MAX_M;
+    if (want_skinny && plan_skinny(A, Bc, C, m, n, k, N, M, V, p)) return p;
     p.kind = Kind::General;
     if (k % 4 != 0 || V % 16 != 0 || 128 % M != 0) return p;
-    const int BV = V % 64 == 0 ? 4 : (V % 32 == 0 ? 2 : 1);
-    if (!aligned(A, 16) || !aligned(Bc, 16) || !aligned(C, 4 * BV)) return p;
+    if (!aligned(A, 16) || !aligned(Bc, 16)) return p;
     // per-stage Bc buffer offsets reach (padded rows) x n x 4 bytes < 32 x n x 4
     if ((int64_t)32 * n * 4 >= (int64_t(1) << 31)) return p;
 
-    // Stage depth: the smallest KA (a multiple of 32 and of M) whose stage
-    // holds at least 16 compressed rows, so every stage carries enough MFMA
-    // work to cover its fixed cost; deeper ones are tried if it does not fit.
+    // Stage depth for the eight-wave tiles: the smallest KA (a multiple of 32
+    // and of M) whose stage holds at least 16 compressed rows, so every stage
+    // carries enough MFMA work to cover its fixed cost; deeper ones are tried
+    // if it does not fit.  The small tiles (four waves or fewer) instead take
+    // the shallowest stage, whose smaller LDS ring lets more workgroups share
+    // a CU.
     int ka_order[3], nka = 0;
     for (int KA : {32, 64, 128})
         if (KA % M == 0 && (KA / M) * N >= 16) ka_order[nka++] = KA;
     for (int KA : {128, 64, 32})
         if (KA % M == 0 && (KA / M) * N < 16) ka_order[nka++] = KA;
-    if (const char *force = std::getenv("NMSPMM_KA")) {  // tuning sweeps only
-        const int ka = std::atoi(force);
-        if (ka == 32 || ka == 64 || ka == 128) { ka_order[0] = ka; nka = 1; }
+    int ka_small[3], nks = 0;
+    for (int KA : {32, 64, 128})
+        if (KA % M == 0) ka_small[nks++] = KA;
+    const int ka_force = env_int("NMSPMM_KA", 0);
+    if (ka_force == 32 || ka_force == 64 || ka_force == 128) {
+        ka_order[0] = ka_small[0] = ka_force;
+        nka = nks = 1;
     }
 
     const TileInfo *cand[8];
-    int nc = preferences(m, n, cand);
-    if (const char *force = std::getenv("NMSPMM_TILE")) {  // tuning sweeps only
-        const TileInfo *t = tile_by_name(force);
+    int nc = preferences(m, n, N, M, cand);
+    if (force_tile) {
+        const TileInfo *t = tile_by_name(force_tile);
         if (t) { cand[0] = t; nc = 1; }
     }
     // first tile shape (in preference order) that some stage depth fits
     const TileInfo *tile = nullptr;
-    int KA = 0, NQ = 0;
+    int KA = 0, NQ = 0, BV = 0;
     for (int j = 0; j < nc && !tile; ++j) {
         if (!cand[j]) continue;
-        for (int i = 0; i < nka && !tile; ++i) {
-            const int nq = stage_nq(ka_order[i], (ka_order[i] / M) * N);
-            if (nq != 0 && tile_ok(*cand[j], BV, ka_order[i], nq, k, V)) {
+        const int bv = bv_for(cand[j]->MI, V);
+        if (bv == 0 || !aligned(C, 4 * bv)) continue;
+        const bool small = cand[j]->waves <= 4;
+        const int *order = small ? ka_small : ka_order;
+        for (int i = 0; i < (small ? nks : nka) && !tile; ++i) {
+            const int nq = stage_nq(order[i], (order[i] / M) * N);
+            if (nq != 0 && tile_ok(*cand[j], bv, order[i], nq, k, V)) {
                 tile = cand[j];
-                KA = ka_order[i];
+                KA = order[i];
                 NQ = nq;
+                BV = bv;
             }
         }
     }
@@ -235,6 +329,23 @@ hipError_t launch_plan(const Plan &p, const float *A, const float *Bc, const uin
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
+    if (p.kind == Kind::Skinny) {
+        SkinnyArgs s;
+        s.A = A;
+        s.Bc = Bc;
+        s.idx = idx;
+        s.C = C;
+        s.m = m;
+        s.n = n;
+        s.k = k;
+        s.N = N;
+        s.M = M;
+        s.V = V;
+        s.splits = p.splits;
+        s.tiles_m = p.tiles_m;
+        s.tiles_n = p.tiles_n;
+        return launch_skinny(p.BV, p.QPW, s, stream);
+    }
     TiledArgs a;
     a.A = A;
     a.Bc = Bc;
@@ -268,9 +379,14 @@ extern "C" const char *nmspmm_kernel_name(int64_t m, int64_t n, int64_t k, int N
     switch (p.kind) {
     case Kind::None: return "none";
     case Kind::General: return "nm_general_kernel";
-    case Kind::Tiled: break;
+    case Kind::Tiled: case Kind::Skinny: break;
     }
     thread_local char buf[96];
+    if (p.kind == Kind::Skinny) {
+        std::snprintf(buf, sizeof buf, "nm_skinny_kernel<bv%d,qpw%d>%s%d", p.BV, p.QPW,
+                      p.splits > 1 ? "+zero,split" : ",split", p.splits);
+        return buf;
+    }
     std::snprintf(buf, sizeof buf, "nm_tiled_kernel<%s,bv%d,ka%d,nq%d>%s%d", p.tile->name, p.BV,
                   p.KA, p.NQ, p.splits > 1 ? "+zero,split" : ",split", p.splits);
     return buf;

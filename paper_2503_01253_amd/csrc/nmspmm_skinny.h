@@ -1,0 +1,31 @@
+// Host-side entry of the streaming kernel for short products (nmspmm_skinny.hip).
+#ifndef NMSPMM_SKINNY_H
+#define NMSPMM_SKINNY_H
+
+#include <hip/hip_runtime_api.h>
+
+#include <cstdint>
+
+namespace nmspmm {
+
+struct SkinnyArgs {
+    const float *A;
+    const float *Bc;
+    const uint8_t *idx;
+    float *C;
+    int64_t m, n, k;
+    int N, M, V;
+    int splits;          // workgroups per output tile along k (>1: atomic adds into a zeroed C)
+    int tiles_m, tiles_n;
+};
+
+int skinny_rows();       // rows of C per workgroup
+int skinny_cols();       // columns of C per workgroup
+
+// BV: columns per lane per B read (1, 2 or 4); QPW: quads per wave per round (1, 2 or 4).
+bool skinny_has(int BV, int QPW);
+hipError_t launch_skinny(int BV, int QPW, const SkinnyArgs &a, hipStream_t stream);
+
+}  // namespace nmspmm
+
+#endif

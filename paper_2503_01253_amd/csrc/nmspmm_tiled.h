@@ -3,42 +3,39 @@
 //
 // One workgroup owns a BM x BN tile of C (and, with split-k, one slice of the
 // k range).  It walks k in stages of KA columns of A (KA/M whole windows,
-// RS = (KA/M)*N compressed rows, padded to RST = 4*NQ rows: MFMA K = 4).  KA
+// RS = (KA/M)*N compressed rows, padded to RST = 4*NQ rows).  KA
 // grows as N/M shrinks so that a stage carries about sixteen compressed rows
 // at every sparsity, the way the paper sizes k_s from the shared-memory budget
-// and N/M (Sec. III-B.1, Eq. 5).  Each stage is brought into a ring of P LDS
-// slots (the double buffer of Sec. III-C.2, deepened to P slots):
-//   A_s : the BM x KA slab of A, row-major.  The whole slab is staged (the
-//         non-packing load of Sec. III-C.1): with random per-block patterns
-//         nearly every column is needed by some block of the tile.  Word c of
-//         row i is stored at word position c ^ (i & 31), so that the sixteen
-//         consecutive rows an MFMA gathers from one column fall in sixteen
-//         different LDS banks.
+// and N/M (Sec. III-B.1, Eq. 5).  Each stage is staged in one of two LDS
+// slots (the double buffer of Sec. III-C.2):
+//   A_s : the BM x KA slab of A, stored k-major (A_s[c][i], rows padded by 4
+//         floats).  The whole slab is staged (the non-packing load of Sec.
+//         III-C.1): with random per-block patterns nearly every column is
+//         needed by some block of the tile.  k-major storage turns the N:M
+//         gather of Eq. 1 into "pick LDS row c", and one 16-byte read gives
+//         a lane RPL = 4 consecutive output rows of the gathered column.  It
+//         goes global -> registers -> LDS: each thread loads a 4 x 4 block
+//         (four 16-byte row pieces) and writes it transposed (four 16-byte
+//         column pieces).
 //   B_s : the RST x BN slab of Bc, row-major (padding rows are zero).
 //   X_s : the RST x (BN/V) offset bytes of D, one zero-extended dword each.
-// All three are filled by buffer->LDS DMA (no register staging); each lane
-// picks the global address whose data belongs at its fixed LDS position,
-// which is how the swizzle is applied.  Out-of-range lanes (ragged m, n, k
-// tails, padding rows) read zero.  Every wave issues the same number of DMA
-// instructions per stage, so "a stage has landed" is a counted vmcnt wait
-// followed by a barrier.
+// B_s and X_s are filled by buffer->LDS DMA.  All global reads go through
+// buffer descriptors whose range makes ragged m / n / k tails and padding
+// rows read zero.  The loads of stage s+1 are issued before stage s is
+// multiplied; the A registers are written to the other slot after it; one
+// barrier per stage.  Inside a stage the offsets of all MFMA K steps are read
+// once (the index prefetch of Sec. III-C.2) and the operands of step j+1 are
+// read while step j is multiplied (the register double buffer of the same
+// section).
 //
-// Schedule (P >= 3): the barrier at the top of iteration s certifies that
-// every wave is done with slot s-1 and that stage s has landed; the DMA of
-// stage s+P-1 then refills slot s-1, so P-1 stages stay in flight behind the
-// one being multiplied.  Inside a stage
-// the offsets of all its quads are read once (the index prefetch of Sec.
-// III-C.2) and the operands of quad q+1 are read while quad q is multiplied
-// (the register double buffer of the same section).  With P == 2 the plain
-// double buffer is used.
-//
-// Contraction: v_mfma_f32_16x16x4_f32 (fp32 in, fp32 accumulate).  Lane l
-// supplies A[l%16][l/16] and B[l/16][l%16] and receives D[4*(l/16)+v][l%16]
-// in element v.  The K index l/16 selects one of four consecutive compressed
-// rows, each with its own gather offset; the 16 columns of one MFMA lie in a
-// column group of CG = 16*BV columns inside one column block, so they share
-// one gather.  A lanes read output row l%16 of a 16-row chunk; B lanes read
-// columns BV*(l%16)+s, s < BV (BV MFMAs per A read).
+// Contraction: fp32 MFMA (fp32 in, fp32 accumulate), v_mfma_f32_16x16x4_f32
+// or v_mfma_f32_32x32x2_f32 (MI = 16 or 32).  Lane l supplies A[l%MI][l/MI]
+// and B[l/MI][l%MI]; the K index l/MI selects one of KG = 64/MI consecutive
+// compressed rows, each with its own gather offset.  The MI columns of one
+// MFMA lie in a column group of CG = MI*BV columns inside one column block,
+// so they share one gather.  A lanes read output rows RPL*(l%MI)+t (t < RPL)
+// of an MI*RPL-row chunk; B lanes read columns BV*(l%MI)+s (s < BV); one A
+// read feeds RPL*BV MFMAs.
 #ifndef NMSPMM_TILED_H
 #define NMSPMM_TILED_H
 
@@ -64,45 +61,46 @@ __device__ __forceinline__ float lane_of(const typename vec_of<W>::type &v, int 
 }
 
 constexpr int LDS_CAPACITY = 160 * 1024;
-constexpr int SWZ = 31;           // word swizzle mask of A_s rows (KA is a multiple of 32)
 
-template <int BM_, int BN_, int WM_, int WN_>
+// MI selects the MFMA: 16 -> v_mfma_f32_16x16x4_f32 (K = 4 compressed rows,
+// 16 lanes per K index), 32 -> v_mfma_f32_32x32x2_f32 (K = 2, 32 lanes per
+// K index).  The 32 x 32 form issues half as many instructions for the same
+// work and keeps the matrix pipe busier; it needs V to be a multiple of 32.
+template <int BM_, int BN_, int WM_, int WN_, int MI_ = 16>
 struct TileCfg {
-    static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_;
+    static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_, MI = MI_;
     static constexpr int NW = (BM / WM) * (BN / WN);
     static constexpr int NT = NW * 64;
-    static constexpr int NRC = WM / 16;         // 16-row MFMA chunks per wave
-    static_assert(WM % 16 == 0 && BM % WM == 0 && BN % WN == 0, "tile shape");
+    static constexpr int KG = 64 / MI;                 // K per MFMA (compressed rows)
+    static constexpr int RPL = WM % (4 * MI) == 0 ? 4 : 1;  // output rows per lane read
+    static constexpr int RCH = MI * RPL;               // rows per MFMA row chunk
+    static constexpr int NRC = WM / RCH;
+    static constexpr int AST = BM + 4;                 // floats per A_s row (k-major)
+    static_assert(MI == 16 || MI == 32, "MFMA shape");
+    static_assert(WM % MI == 0 && BM % WM == 0 && BN % WN == 0, "tile shape");
 };
 
 // Per-instantiation constants (tile x column-group width x stage shape).
 template <class T, int BV, int KA, int NQ>
 struct Shape {
-    static constexpr int CG = 16 * BV;
+    static constexpr int CG = T::MI * BV;
     static constexpr int NCG = T::WN / CG;
     static constexpr int RST = 4 * NQ;                 // padded rows per stage
     static constexpr int QBMAX = T::BN / CG;           // column blocks per tile, at most
-    static constexpr int A_ROW = KA * 4;               // bytes per A_s row
-    static constexpr int A_BYTES = T::BM * A_ROW;
-    static constexpr int B_BYTES = RST * T::BN * 4;
-    static constexpr int X_BYTES = T::NT * 4;
-    static constexpr int STAGE_BYTES = A_BYTES + B_BYTES + X_BYTES;
-    // DMA instructions per wave per stage: A in dwords (word-level swizzle),
-    // B in 16-byte pieces when the slab divides evenly, one byte of D per lane
-    static constexpr int A_CNT = A_BYTES / (T::NT * 4);
-    static constexpr int B_LANE = B_BYTES / T::NT;
+    static constexpr int A_FLOATS = KA * T::AST;
+    static constexpr int B_FLOATS = RST * T::BN;
+    static constexpr int X_INTS = T::NT;
+    static constexpr int SLOT_BYTES = 4 * (A_FLOATS + B_FLOATS + X_INTS);
+    // A: 32 x 32 chunks, one per wave at a time, each thread a 4 x 4 block
+    static constexpr int A_CHUNKS = ((T::BM + 31) / 32) * (KA / 32);
+    static constexpr int ACH = (A_CHUNKS + T::NW - 1) / T::NW;
+    // B DMA: 16-byte pieces when the slab divides evenly, else dwords
+    static constexpr int B_LANE = B_FLOATS * 4 / T::NT;
     static constexpr int B_W = B_LANE % 16 == 0 ? 16 : 4;
     static constexpr int B_CNT = B_LANE / B_W;
-    static constexpr int LOADS = A_CNT + B_CNT + 1;
-    // ring depth: what LDS holds, at most 6, and few enough stages in flight
-    // that a wait count (stages x LOADS) fits the 6-bit vmcnt
-    static constexpr int P_LDS = LDS_CAPACITY / STAGE_BYTES;
-    static constexpr int P_CNT = 2 + 63 / LOADS;
-    static constexpr int P = P_LDS < P_CNT ? (P_LDS < 6 ? P_LDS : 6) : (P_CNT < 6 ? P_CNT : 6);
-    static constexpr bool FITS = P >= 2 && KA % 32 == 0 && T::WN % CG == 0 &&
-                                 RST * QBMAX <= T::NT && A_BYTES % (T::NT * 4) == 0 &&
-                                 B_BYTES % T::NT == 0 && B_LANE % 4 == 0 && A_CNT >= 1 &&
-                                 B_CNT >= 1 && (P - 2) * LOADS < 64;
+    static constexpr bool FITS = 2 * SLOT_BYTES <= LDS_CAPACITY && KA % 32 == 0 &&
+                                 T::WN % CG == 0 && RST * QBMAX <= T::NT &&
+                                 (B_FLOATS * 4) % T::NT == 0 && B_LANE % 4 == 0 && B_CNT >= 1;
 };
 
 struct TiledArgs {
@@ -167,29 +165,14 @@ __device__ __forceinline__ void lds_dma(__amdgpu_buffer_rsrc_t rsrc, void *dst, 
         __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void *)dst, 1, (int)off, 0, 0, 0);
 }
 
-// Wait until at most later_stages * LOADS DMA instructions of this wave are
-// outstanding (s_waitcnt simm16 on gfx9: vmcnt[3:0] | expcnt[6:4] |
-// lgkmcnt[11:8] | vmcnt[5:4] << 14; expcnt and lgkmcnt left at their maxima).
-template <int LOADS, int MAXL>
-__device__ __forceinline__ void wait_vm(int later_stages)
-{
-#define NMSPMM_VM(c) __builtin_amdgcn_s_waitcnt(((c) & 15) | (7 << 4) | (15 << 8) | (((c) >> 4) << 14))
-    static_assert(MAXL <= 4 && MAXL * LOADS < 64, "ring depth");
-    if constexpr (MAXL >= 4) { if (later_stages >= 4) { NMSPMM_VM(4 * LOADS); return; } }
-    if constexpr (MAXL >= 3) { if (later_stages >= 3) { NMSPMM_VM(3 * LOADS); return; } }
-    if constexpr (MAXL >= 2) { if (later_stages >= 2) { NMSPMM_VM(2 * LOADS); return; } }
-    if constexpr (MAXL >= 1) { if (later_stages >= 1) { NMSPMM_VM(1 * LOADS); return; } }
-    NMSPMM_VM(0);
-#undef NMSPMM_VM
-}
-
-// Workgroup barrier without a memory fence: LDS visibility is established by
-// the explicit vmcnt wait before it and the lgkmcnt(0) inside it; the empty
-// asm statements keep the compiler from moving memory accesses across it.
-__device__ __forceinline__ void block_sync()
+// Workgroup barrier after this wave's outstanding global loads and DMA have
+// completed (vmcnt(0)) and its LDS accesses have too (lgkmcnt(0)).  No memory
+// fence beyond that is needed; the empty asm statements keep the compiler
+// from moving memory accesses across it.
+__device__ __forceinline__ void stage_sync()
 {
     asm volatile("" ::: "memory");
-    __builtin_amdgcn_s_waitcnt((15) | (7 << 4) | (0 << 8) | (3 << 14));  // lgkmcnt(0)
+    __builtin_amdgcn_s_waitcnt(0 | (7 << 4) | (0 << 8) | (0 << 14));  // vmcnt(0) lgkmcnt(0)
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
 }
@@ -198,12 +181,13 @@ template <class T, int BV, int KA, int NQ>
 __global__ __launch_bounds__(T::NT) void nm_tiled_kernel(TiledArgs p)
 {
     using S = Shape<T, BV, KA, NQ>;
-    constexpr int BM = T::BM, BN = T::BN, WM = T::WM, WN = T::WN, NW = T::NW, NRC = T::NRC;
-    constexpr int CG = S::CG, NCG = S::NCG, RST = S::RST, P = S::P, LOADS = S::LOADS;
-    constexpr int A_ROW = S::A_ROW;
+    constexpr int BM = T::BM, BN = T::BN, WM = T::WM, WN = T::WN, NW = T::NW;
+    constexpr int RPL = T::RPL, RCH = T::RCH, NRC = T::NRC, AST = T::AST;
+    constexpr int CG = S::CG, NCG = S::NCG, RST = S::RST, ACH = S::ACH;
     typedef typename vec_of<BV>::type bvec;
+    typedef typename vec_of<RPL>::type avec;
 
-    __shared__ __align__(16) unsigned char lds[P * S::STAGE_BYTES];
+    __shared__ __align__(16) unsigned char lds[2 * S::SLOT_BYTES];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     int tm, tn, split;
@@ -226,18 +210,48 @@ __global__ __launch_bounds__(T::NT) void nm_tiled_kernel(TiledArgs p)
 #pragma unroll
     for (int cg = 0; cg < NCG; ++cg) blk[cg] = (int)((col0 + wn * WN + cg * CG) / V - b_first);
 
-    // ---- per-lane DMA source offsets that do not change between stages ----
+    // ---- A: global -> registers (4 x 4 blocks) -> LDS, k-major ----
+    // In a 32 x 32 chunk, lane l owns rows 4*(l%8)+t (t < 4) and columns
+    // 4*(l/8)..+3: each load instruction covers 8 rows x 128 bytes.
+    const int r8 = lane & 7, c8 = lane >> 3;
     const int rows_valid = (int)min<int64_t>(BM, m - row0);
     const __amdgpu_buffer_rsrc_t a_rsrc =
         make_rsrc(p.A + row0 * k, (uint32_t)((int64_t)rows_valid * k * 4));
-    // A DMA i of this wave fills word position (i*NW + wave)*64 + lane of
-    // A_s: row a_row0 + i*AR (AR = NT/KA, a_row0 < AR) at in-row slot a_slot,
-    // which holds column a_slot ^ (row & SWZ) = a_c0 ^ ((i*AR) & SWZ).
-    constexpr int AR = T::NT / KA;
-    static_assert(T::NT % KA == 0 && (AR & (AR - 1)) == 0, "A DMA rows");
-    const int a_row0 = (wave * 64 + lane) / KA, a_slot = (wave * 64 + lane) % KA;
-    const int a_c0 = a_slot ^ (a_row0 & SWZ);
-    const uint32_t a_rowbase = (uint32_t)(a_row0 * k * 4);
+    f32x4 ra[ACH][4];
+    auto load_a = [&](int s) {
+        const int64_t kc0 = (int64_t)s * KA;
+#pragma unroll
+        for (int ch = 0; ch < ACH; ++ch) {
+            const int chunk = wave + ch * NW;
+            const int rbase = (chunk % ((BM + 31) / 32)) * 32, cbase = (chunk / ((BM + 31) / 32)) * 32;
+            const int64_t kcol = kc0 + cbase + 4 * c8;
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+                const int r = rbase + 4 * r8 + t;
+                const bool ok = chunk < S::A_CHUNKS && r < BM && kcol < k;
+                const uint32_t off = ok ? (uint32_t)((r * k + kcol) * 4) : OOB;
+                // the buffer load returns raw dwords; reinterpret them as floats
+                ra[ch][t] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(a_rsrc, (int)off, 0, 0));
+            }
+        }
+    };
+    auto store_a = [&](int slot) {
+        float *As = reinterpret_cast<float *>(lds + slot * S::SLOT_BYTES);
+#pragma unroll
+        for (int ch = 0; ch < ACH; ++ch) {
+            const int chunk = wave + ch * NW;
+            const int rbase = (chunk % ((BM + 31) / 32)) * 32, cbase = (chunk / ((BM + 31) / 32)) * 32;
+            if (chunk < S::A_CHUNKS && rbase + 4 * r8 < BM) {
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    const f32x4 v = {ra[ch][0][c], ra[ch][1][c], ra[ch][2][c], ra[ch][3][c]};
+                    *reinterpret_cast<f32x4 *>(As + (cbase + 4 * c8 + c) * AST + rbase + 4 * r8) = v;
+                }
+            }
+        }
+    };
+
+    // ---- B and D offsets: buffer -> LDS DMA ----
     uint32_t b_off[S::B_CNT];
     bool b_ok[S::B_CNT];
 #pragma unroll
@@ -250,84 +264,72 @@ __global__ __launch_bounds__(T::NT) void nm_tiled_kernel(TiledArgs p)
     const int x_ul = tid / QB, x_bl = tid % QB;
     const bool x_ok = tid < RST * QB && x_ul < RS && b_first + x_bl < q;
     const uint32_t x_off = (uint32_t)(x_ul * q + b_first + x_bl);
-
-    auto issue_stage = [&](int s, int slot) {
-        unsigned char *base = lds + slot * S::STAGE_BYTES;
-        const int64_t kc0 = (int64_t)s * KA;
-        const bool full = kc0 + KA <= k;   // uniform; only a last, partial stage is not
-#pragma unroll
-        for (int i = 0; i < S::A_CNT; ++i) {
-            const int col = a_c0 ^ ((i * AR) & SWZ);
-            // the stage- and DMA-dependent part is made an opaque scalar so that
-            // the per-lane offsets are formed here, not hoisted out of the loop
-            const uint32_t su = __builtin_amdgcn_readfirstlane((uint32_t)((i * AR * k + kc0) * 4));
-            const uint32_t off = a_rowbase + (uint32_t)col * 4u + su;
-            lds_dma<4>(a_rsrc, base + (i * NW + wave) * 64 * 4, full || kc0 + col < k ? off : OOB);
-        }
+    auto dma_bx = [&](int s, int slot) {
+        unsigned char *bs = lds + slot * S::SLOT_BYTES + 4 * S::A_FLOATS;
         const int64_t u0 = (int64_t)s * RS;
         const int64_t rows_left = min<int64_t>(RS, w - u0);
         const __amdgpu_buffer_rsrc_t b_rsrc = make_rsrc(p.Bc + u0 * n, (uint32_t)(rows_left * n * 4));
 #pragma unroll
         for (int i = 0; i < S::B_CNT; ++i)
-            lds_dma<S::B_W>(b_rsrc, base + S::A_BYTES + (i * NW + wave) * 64 * S::B_W,
-                            b_ok[i] ? b_off[i] : OOB);
+            lds_dma<S::B_W>(b_rsrc, bs + (i * NW + wave) * 64 * S::B_W, b_ok[i] ? b_off[i] : OOB);
         const __amdgpu_buffer_rsrc_t x_rsrc = make_rsrc(p.idx + u0 * q, (uint32_t)(rows_left * q));
-        lds_dma<1>(x_rsrc, base + S::A_BYTES + S::B_BYTES + wave * 64 * 4, x_ok ? x_off : OOB);
+        lds_dma<1>(x_rsrc, bs + 4 * S::B_FLOATS + wave * 64 * 4, x_ok ? x_off : OOB);
     };
 
-    f32x4 acc[NCG][NRC][BV];
+    constexpr int MI = T::MI, KG = T::KG;
+    constexpr int NKS = RST / KG;                   // MFMA K steps per stage
+    constexpr int NACC = MI * MI / 64;              // accumulator floats per lane per MFMA
+    typedef float accv __attribute__((ext_vector_type(NACC)));
+    accv acc[NCG][NRC][RPL][BV];
 #pragma unroll
     for (int cg = 0; cg < NCG; ++cg)
 #pragma unroll
         for (int rc = 0; rc < NRC; ++rc)
 #pragma unroll
-            for (int s = 0; s < BV; ++s) acc[cg][rc][s] = f32x4{0.f, 0.f, 0.f, 0.f};
+            for (int t = 0; t < RPL; ++t)
+#pragma unroll
+                for (int s = 0; s < BV; ++s)
+#pragma unroll
+                    for (int e = 0; e < NACC; ++e) acc[cg][rc][t][s][e] = 0.f;
 
-    const int r = lane & 15, kq = lane >> 4;
+    const int r = lane % MI, kq = lane / MI;        // lane's row/column index, K index
     const int gps = KA / M;                         // windows per stage
-    const int arow = wm * WM + r;                   // this lane's A row in chunk 0
-    const int fsw = arow & SWZ;                     // its swizzle; chunk rc adds 16*rc
 
-    // Gather offsets of one stage: byte offset inside the lane's A_s row for
-    // even chunks (odd chunks sit 16 rows further, where the swizzle differs
-    // in word bit 4, i.e. byte bit 6).
-    int aoff[NQ][NCG];
+    // Gather offsets of one stage: byte offset of the A_s row (column of A)
+    // each of this lane's compressed rows reads, per column group.
+    int aoff[NKS][NCG];
     auto prep_offsets = [&](int slot) {
-        const unsigned char *base = lds + slot * S::STAGE_BYTES;
-        const int *Xs = reinterpret_cast<const int *>(base + S::A_BYTES + S::B_BYTES);
+        const int *Xs = reinterpret_cast<const int *>(lds + slot * S::SLOT_BYTES +
+                                                      4 * (S::A_FLOATS + S::B_FLOATS));
 #pragma unroll
-        for (int qd = 0; qd < NQ; ++qd)
+        for (int ks = 0; ks < NKS; ++ks)
 #pragma unroll
-            for (int cg = 0; cg < NCG; ++cg) aoff[qd][cg] = Xs[(4 * qd + kq) * QB + blk[cg]];
+            for (int cg = 0; cg < NCG; ++cg) aoff[ks][cg] = Xs[(KG * ks + kq) * QB + blk[cg]];
 #pragma unroll
-        for (int qd = 0; qd < NQ; ++qd) {
+        for (int ks = 0; ks < NKS; ++ks) {
             // window of this compressed row inside the stage; padding rows
             // (ul >= RS, zero in B_s) are clamped to the last window so that
             // they still address finite A_s data
-            const int ul = 4 * qd + kq;
+            const int ul = KG * ks + kq;
             const int window = min(ul / N, gps - 1) * M;
 #pragma unroll
-            for (int cg = 0; cg < NCG; ++cg) {
-                const int c = window + min(aoff[qd][cg], M - 1);   // column of A_s gathered
-                aoff[qd][cg] = (c ^ fsw) * 4;
-            }
+            for (int cg = 0; cg < NCG; ++cg)
+                aoff[ks][cg] = (window + min(aoff[ks][cg], M - 1)) * (AST * 4);
         }
     };
 
-    float a[2][NCG][NRC];
+    avec a[2][NCG][NRC];
     bvec b[2][NCG];
-    auto fetch = [&](int slot, int qd, int sl) {
-        const unsigned char *base = lds + slot * S::STAGE_BYTES;
-        const unsigned char *Ab = base + arow * A_ROW;
-        const float *Bcol = reinterpret_cast<const float *>(base + S::A_BYTES) + wn * WN + BV * r;
+    auto fetch = [&](int slot, int ks, int sl) {
+        const unsigned char *base = lds + slot * S::SLOT_BYTES;
+        const unsigned char *Ab = base + (wm * WM + RPL * r) * 4;
+        const float *Bcol = reinterpret_cast<const float *>(base + 4 * S::A_FLOATS) + wn * WN + BV * r;
 #pragma unroll
         for (int cg = 0; cg < NCG; ++cg) {
 #pragma unroll
-            for (int rc = 0; rc < NRC; ++rc) {
-                const int o = (rc & 1) ? (aoff[qd][cg] ^ 64) : aoff[qd][cg];
-                a[sl][cg][rc] = *reinterpret_cast<const float *>(Ab + rc * 16 * A_ROW + o);
-            }
-            b[sl][cg] = *reinterpret_cast<const bvec *>(Bcol + (4 * qd + kq) * BN + cg * CG);
+            for (int rc = 0; rc < NRC; ++rc)
+                a[sl][cg][rc] = *reinterpret_cast<const avec *>(Ab + aoff[ks][cg] + rc * RCH * 4);
+            b[sl][cg] = *reinterpret_cast<const bvec *>(Bcol + (KG * ks + kq) * BN + cg * CG);
         }
     };
     auto mma = [&](int sl) {
@@ -336,62 +338,53 @@ __global__ __launch_bounds__(T::NT) void nm_tiled_kernel(TiledArgs p)
 #pragma unroll
             for (int rc = 0; rc < NRC; ++rc)
 #pragma unroll
-                for (int s = 0; s < BV; ++s)
-                    acc[cg][rc][s] = __builtin_amdgcn_mfma_f32_16x16x4f32(
-                        a[sl][cg][rc], lane_of<BV>(b[sl][cg], s), acc[cg][rc][s], 0, 0, 0);
+                for (int t = 0; t < RPL; ++t)
+#pragma unroll
+                    for (int s = 0; s < BV; ++s) {
+                        if constexpr (MI == 16)
+                            acc[cg][rc][t][s] = __builtin_amdgcn_mfma_f32_16x16x4f32(
+                                lane_of<RPL>(a[sl][cg][rc], t), lane_of<BV>(b[sl][cg], s),
+                                acc[cg][rc][t][s], 0, 0, 0);
+                        else
+                            acc[cg][rc][t][s] = __builtin_amdgcn_mfma_f32_32x32x2f32(
+                                lane_of<RPL>(a[sl][cg][rc], t), lane_of<BV>(b[sl][cg], s),
+                                acc[cg][rc][t][s], 0, 0, 0);
+                    }
     };
 
-    if constexpr (P >= 3) {
-        // ---- P-slot ring: P-1 stages in flight behind the one multiplied ----
-#pragma unroll
-        for (int j = 0; j < P - 1; ++j)
-            if (j < nst) issue_stage(s_begin + j, j);
-        if (nst > 0) {
-            wait_vm<LOADS, P - 2>(min(nst - 1, P - 2));   // stage 0 landed
-            block_sync();
+    // ---- double-buffered stages, one barrier each ----
+    if (nst > 0) {
+        load_a(s_begin);
+        dma_bx(s_begin, 0);
+        store_a(0);
+        stage_sync();
+    }
+    for (int it = 0; it < nst; ++it) {
+        const int cur = it & 1;
+        const bool next = it + 1 < nst;
+        if (next) {
+            load_a(s_begin + it + 1);
+            dma_bx(s_begin + it + 1, cur ^ 1);
         }
-        for (int it = 0; it < nst; ++it) {
-            const int slot = it % P;
-            if (it > 0) {
-                wait_vm<LOADS, P - 2>(min(nst - 1 - it, P - 2));  // stage it landed
-                block_sync();
-            }
-            prep_offsets(slot);
-            fetch(slot, 0, 0);
-            if (it + P - 1 < nst) issue_stage(s_begin + it + P - 1, (it + P - 1) % P);
+        prep_offsets(cur);
+        fetch(cur, 0, 0);
 #pragma unroll
-            for (int qd = 0; qd < NQ; ++qd) {
-                const int sl = qd & 1;
-                if (qd + 1 < NQ) fetch(slot, qd + 1, sl ^ 1);
-                // keep the next LDS reads ahead of this quad's MFMAs
-                __builtin_amdgcn_sched_barrier(0);
-                mma(sl);
-                __builtin_amdgcn_sched_barrier(0);
-            }
+        for (int ks = 0; ks < NKS; ++ks) {
+            const int sl = ks & 1;
+            if (ks + 1 < NKS) fetch(cur, ks + 1, sl ^ 1);
+            // keep the next LDS reads ahead of this step's MFMAs
+            __builtin_amdgcn_sched_barrier(0);
+            mma(sl);
+            __builtin_amdgcn_sched_barrier(0);
         }
-    } else {
-        // ---- plain double buffer ----
-        if (nst > 0) issue_stage(s_begin, 0);
-        for (int it = 0; it < nst; ++it) {
-            const int slot = it & 1;
-            wait_vm<LOADS, 0>(0);
-            block_sync();
-            if (it + 1 < nst) issue_stage(s_begin + it + 1, slot ^ 1);
-            prep_offsets(slot);
-            fetch(slot, 0, 0);
-#pragma unroll
-            for (int qd = 0; qd < NQ; ++qd) {
-                const int sl = qd & 1;
-                if (qd + 1 < NQ) fetch(slot, qd + 1, sl ^ 1);
-                __builtin_amdgcn_sched_barrier(0);
-                mma(sl);
-                __builtin_amdgcn_sched_barrier(0);
-            }
-        }
+        if (next) store_a(cur ^ 1);
+        stage_sync();
     }
 
-    // ---- epilogue: lane l holds rows 4*(l/16)+v of each 16-row chunk and
-    // columns BV*(l%16)+s of each column group ----
+    // ---- epilogue.  16x16x4: element e of lane l is row 4*(l/16)+e of the
+    // MFMA tile; 32x32x2: row 8*(e/4) + 4*(l/32) + e%4.  The MFMA tile row i
+    // is output row RPL*i+t of its row chunk; its column is BV*(l%MI)+s of
+    // the column group. ----
 #pragma unroll
     for (int cg = 0; cg < NCG; ++cg) {
         const int64_t col = col0 + wn * WN + cg * CG + BV * r;
@@ -399,24 +392,27 @@ __global__ __launch_bounds__(T::NT) void nm_tiled_kernel(TiledArgs p)
 #pragma unroll
         for (int rc = 0; rc < NRC; ++rc)
 #pragma unroll
-            for (int v = 0; v < 4; ++v) {
-                const int64_t row = row0 + wm * WM + rc * 16 + 4 * kq + v;
-                if (row >= m) continue;
-                float *dst = p.C + row * n + col;
-                if (p.splits == 1) {
-                    bvec out;
-                    if constexpr (BV == 1) {
-                        out = acc[cg][rc][0][v];
+            for (int e = 0; e < NACC; ++e)
+#pragma unroll
+                for (int t = 0; t < RPL; ++t) {
+                    const int i = MI == 16 ? 4 * kq + e : 8 * (e / 4) + 4 * kq + (e % 4);
+                    const int64_t row = row0 + wm * WM + rc * RCH + RPL * i + t;
+                    if (row >= m) continue;
+                    float *dst = p.C + row * n + col;
+                    if (p.splits == 1) {
+                        bvec out;
+                        if constexpr (BV == 1) {
+                            out = acc[cg][rc][t][0][e];
+                        } else {
+#pragma unroll
+                            for (int s = 0; s < BV; ++s) out[s] = acc[cg][rc][t][s][e];
+                        }
+                        *reinterpret_cast<bvec *>(dst) = out;
                     } else {
 #pragma unroll
-                        for (int s = 0; s < BV; ++s) out[s] = acc[cg][rc][s][v];
+                        for (int s = 0; s < BV; ++s) unsafeAtomicAdd(dst + s, acc[cg][rc][t][s][e]);
                     }
-                    *reinterpret_cast<bvec *>(dst) = out;
-                } else {
-#pragma unroll
-                    for (int s = 0; s < BV; ++s) unsafeAtomicAdd(dst + s, acc[cg][rc][s][v]);
                 }
-            }
     }
 }
 

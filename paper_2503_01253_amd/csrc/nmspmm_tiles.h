@@ -17,8 +17,10 @@ NMSPMM_DECLARE_TILE(128x512)
 NMSPMM_DECLARE_TILE(128x128)
 NMSPMM_DECLARE_TILE(64x512)
 NMSPMM_DECLARE_TILE(16x512)
-NMSPMM_DECLARE_TILE(256x256w16)
-NMSPMM_DECLARE_TILE(128x512w16)
+NMSPMM_DECLARE_TILE(256x256m32)
+NMSPMM_DECLARE_TILE(128x512m32)
+NMSPMM_DECLARE_TILE(128x128m32)
+NMSPMM_DECLARE_TILE(64x512m32)
 
 #undef NMSPMM_DECLARE_TILE
 

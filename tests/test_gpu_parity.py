@@ -77,6 +77,14 @@ SMALL = [
     (20, 256, 512, 20, 32, 32),
     (40, 320, 640, 5, 32, 64),
     (130, 1024, 2048, 4, 32, 64),
+    # short products (streaming kernel): ragged column tiles, w not a
+    # multiple of 4, wide windows, uneven k splits
+    (13, 40, 272, 3, 8, 16),
+    (9, 1000, 320, 7, 8, 32),
+    (16, 2048, 640, 4, 32, 128),
+    (11, 768, 1536, 5, 256, 256),
+    (2, 4096, 96, 16, 32, 32),
+    (16, 512, 4096, 4, 32, 64),
 ]
 
 
@@ -188,3 +196,28 @@ def test_out_of_range_offsets_stay_in_bounds():
     idx[::3, ::2] = 255
     C = gpu_run(A, Bc, idx, m, n, k, N, M, V)
     assert np.isfinite(C).all()
+
+
+TILES = ["256x256", "128x512", "128x128", "64x512", "16x512",
+         "256x256m32", "128x512m32", "128x128m32", "64x512m32", "skinny"]
+FORCED = [
+    (300, 256, 1088, 8, 32, 32),
+    (130, 384, 1024, 4, 32, 64),
+    (70, 128, 640, 16, 32, 128),
+    (200, 96, 576, 12, 32, 64),
+]
+
+
+@pytest.mark.parametrize("tile", TILES)
+@pytest.mark.parametrize("shape", FORCED, ids=lambda s: "x".join(map(str, s)))
+def test_every_tile_shape_exact(tile, shape, monkeypatch):
+    """Each tile shape the dispatcher can pick, forced on ragged problems
+    with small-integer data (exact in any summation order)."""
+    m, k, n, N, M, V = shape
+    monkeypatch.setenv("NMSPMM_TILE", tile)
+    name = nm.nmspmm_kernel_name(m, n, k, N, M, V)
+    if f"<{tile}," not in name and not (tile == "skinny" and name.startswith("nm_skinny")):
+        pytest.skip(f"{tile} does not fit {shape} ({name})")
+    C, C_ref, _ = parity(m, k, n, N, M, V, "int", seed=7 + m + n)
+    assert bool(np.array_equal(C.astype(np.float64), C_ref)), \
+        f"{name}: {int(np.count_nonzero(C.astype(np.float64) != C_ref))} outputs differ"
