@@ -101,7 +101,7 @@ struct Plan {
     Kind kind = Kind::None;
     const TileInfo *tile = nullptr;
     int BV = 0, KA = 0, NQ = 0, RS = 0, stages = 0, splits = 1, tiles_m = 0, tiles_n = 0;
-    int QPW = 0;
+    int QPW = 0, COLS = 0, CW = 0;   // streaming kernel only
 };
 
 bool aligned(const void *p, int bytes) { return (reinterpret_cast<uintptr_t>(p) % bytes) == 0; }
@@ -175,9 +175,11 @@ int preferences(int64_t m, int64_t n, int N, int M, const TileInfo **out)
     return c;
 }
 
-// Rows of C up to which the streaming kernel is used (it re-reads Bc once
-// per 16 rows, the tiled kernel once per 128 or more).
-constexpr int64_t SKINNY_MAX_M = 16;
+// Rows of C up to which the streaming kernel is used.  It re-reads Bc once
+// per 16 rows (mostly from L2 and the Infinity Cache), the tiled kernel once
+// per 128 or more; on MI355X the streaming kernel is faster up to 128 rows
+// at k = n = 8192.
+constexpr int64_t SKINNY_MAX_M = 128;
 
 int env_int(const char *name, int fallback)  // tuning sweeps only
 {
@@ -186,32 +188,42 @@ int env_int(const char *name, int fallback)  // tuning sweeps only
 }
 
 // Streaming kernel for short products: every Bc value is loaded once per
-// 16 rows of C straight into MFMA operands; k is split across workgroups
-// until the grid has about one workgroup per CU.
+// 16 rows of C straight into MFMA operands and the A slice is staged in LDS;
+// k is split across workgroups until the grid has about one workgroup per CU.
 bool plan_skinny(const float *A, const float *Bc, const float *C, int64_t m, int64_t n, int64_t k,
                  int N, int M, int V, Plan &p)
 {
-    if (V % 16 != 0 || !aligned(A, 4) || !aligned(Bc, 16) || !aligned(C, 16)) return false;
+    if (V % 16 != 0 || M % 4 != 0) return false;
+    if (!aligned(A, 16) || !aligned(Bc, 16) || !aligned(C, 16)) return false;
     // buffer offsets: 16 rows of A and 4 rows of Bc per resource
     if ((int64_t)skinny_rows() * k * 4 >= (int64_t(1) << 31)) return false;
     if ((int64_t)4 * n * 4 >= (int64_t(1) << 31)) return false;
-    const int bv = bv_for(16, V);
+    // 256 columns per workgroup when that already gives a workgroup per CU,
+    // else 128 (and split-k for the rest)
     const int64_t tiles_m = (m + skinny_rows() - 1) / skinny_rows();
-    const int64_t tiles_n = (n + skinny_cols() - 1) / skinny_cols();
+    int cols = tiles_m * ((n + 255) / 256) >= 256 ? 256 : 128;
+    const int fc = env_int("NMSPMM_SKCOLS", 0);
+    if (fc == 32 || fc == 64 || fc == 128 || fc == 256) cols = fc;
+    const int bv = std::min(bv_for(16, V), cols / 16);
+    const int64_t tiles_n = (n + cols - 1) / cols;
     if (tiles_m * tiles_n > (1 << 24)) return false;
-    const int64_t w = (k / M) * N, quads = (w + 3) / 4, ntiles = tiles_m * tiles_n;
-    // at least one quad per wave and split
-    int64_t splits = std::max<int64_t>(1, std::min<int64_t>((256 + ntiles - 1) / ntiles, quads / 8));
-    splits = std::min<int64_t>(splits, 64);
+    const int64_t G = k / M, ntiles = tiles_m * tiles_n;
+    // about one workgroup per CU, but at least 32 compressed rows (one quad
+    // per wave) per workgroup
+    int64_t splits = std::min<int64_t>((256 + ntiles - 1) / ntiles, G * N / 32);
+    splits = std::max<int64_t>(1, std::min<int64_t>(splits, 64));
     const int fs = env_int("NMSPMM_SPLITS", 0);
-    if (fs >= 1) splits = std::min<int64_t>(fs, std::max<int64_t>(quads, 1));
-    int qpw = bv == 4 ? 4 : 2;
+    if (fs >= 1) splits = std::min<int64_t>(fs, std::max<int64_t>(G, 1));
+    // longer runs per wave when each workgroup walks all of k
+    int qpw = splits == 1 && skinny_has(bv, 4, cols) ? 4 : skinny_has(bv, 2, cols) ? 2 : 1;
     const int fq = env_int("NMSPMM_QPW", 0);
-    if (skinny_has(bv, fq)) qpw = fq;
-    if (ntiles * splits > INT32_MAX) return false;
+    if (skinny_has(bv, fq, cols)) qpw = fq;
+    if (!skinny_has(bv, qpw, cols) || ntiles * splits > INT32_MAX) return false;
     p.kind = Kind::Skinny;
     p.BV = bv;
     p.QPW = qpw;
+    p.COLS = cols;
+    p.CW = skinny_chunk_cols() / M;
     p.splits = (int)splits;
     p.tiles_m = (int)tiles_m;
     p.tiles_n = (int)tiles_n;
@@ -344,7 +356,8 @@ hipError_t launch_plan(const Plan &p, const float *A, const float *Bc, const uin
         s.splits = p.splits;
         s.tiles_m = p.tiles_m;
         s.tiles_n = p.tiles_n;
-        return launch_skinny(p.BV, p.QPW, s, stream);
+        s.cw = p.CW;
+        return launch_skinny(p.BV, p.QPW, p.COLS, s, stream);
     }
     TiledArgs a;
     a.A = A;
@@ -383,7 +396,7 @@ extern "C" const char *nmspmm_kernel_name(int64_t m, int64_t n, int64_t k, int N
     }
     thread_local char buf[96];
     if (p.kind == Kind::Skinny) {
-        std::snprintf(buf, sizeof buf, "nm_skinny_kernel<bv%d,qpw%d>%s%d", p.BV, p.QPW,
+        std::snprintf(buf, sizeof buf, "nm_skinny_kernel<c%d,bv%d,qpw%d>%s%d", p.COLS, p.BV, p.QPW,
                       p.splits > 1 ? "+zero,split" : ",split", p.splits);
         return buf;
     }

@@ -17,14 +17,17 @@ struct SkinnyArgs {
     int N, M, V;
     int splits;          // workgroups per output tile along k (>1: atomic adds into a zeroed C)
     int tiles_m, tiles_n;
+    int cw;              // windows per staged chunk of A: cw * M <= skinny_chunk_cols()
 };
 
-int skinny_rows();       // rows of C per workgroup
-int skinny_cols();       // columns of C per workgroup
+int skinny_rows();        // rows of C per workgroup
+int skinny_chunk_cols();  // columns of A per staged chunk
 
-// BV: columns per lane per B read (1, 2 or 4); QPW: quads per wave per round (1, 2 or 4).
-bool skinny_has(int BV, int QPW);
-hipError_t launch_skinny(int BV, int QPW, const SkinnyArgs &a, hipStream_t stream);
+// BV: columns per lane per B read (1, 2 or 4); QPW: quads per wave per round
+// (1, 2 or 4); COLS: columns of C per workgroup (32, 64, 128 or 256).  A must be
+// 16-byte aligned and M a multiple of 4 (16-byte loads of A along k).
+bool skinny_has(int BV, int QPW, int COLS);
+hipError_t launch_skinny(int BV, int QPW, int COLS, const SkinnyArgs &a, hipStream_t stream);
 
 }  // namespace nmspmm
 

@@ -221,3 +221,31 @@ def test_every_tile_shape_exact(tile, shape, monkeypatch):
     C, C_ref, _ = parity(m, k, n, N, M, V, "int", seed=7 + m + n)
     assert bool(np.array_equal(C.astype(np.float64), C_ref)), \
         f"{name}: {int(np.count_nonzero(C.astype(np.float64) != C_ref))} outputs differ"
+
+
+SKINNY = [
+    (16, 2048, 640, 4, 32, 64),     # 2 chunks of A per split, ragged column tile
+    (13, 3072, 384, 3, 8, 16),      # 3 chunks of 1024 columns, w not a multiple of 4
+    (7, 1280, 512, 5, 256, 128),    # M = 256: 4 windows per chunk
+    (40, 512, 256, 8, 32, 32),      # several row tiles, rows past m
+]
+
+
+@pytest.mark.parametrize("cols,qpw", [(256, 1), (256, 2), (128, 1), (128, 2), (128, 4),
+                                      (64, 1), (64, 2), (64, 4), (32, 1), (32, 2), (32, 4)])
+@pytest.mark.parametrize("splits", [1, 3])
+@pytest.mark.parametrize("shape", SKINNY, ids=lambda s: "x".join(map(str, s)))
+def test_skinny_variants_exact(shape, splits, cols, qpw, monkeypatch):
+    """Every streaming-kernel variant (columns per workgroup, quads per wave,
+    k split), forced, on small-integer data (exact in any summation order)."""
+    m, k, n, N, M, V = shape
+    monkeypatch.setenv("NMSPMM_TILE", "skinny")
+    monkeypatch.setenv("NMSPMM_SKCOLS", str(cols))
+    monkeypatch.setenv("NMSPMM_QPW", str(qpw))
+    monkeypatch.setenv("NMSPMM_SPLITS", str(splits))
+    name = nm.nmspmm_kernel_name(m, n, k, N, M, V)
+    if not name.startswith(f"nm_skinny_kernel<c{cols},") or f"qpw{qpw}>" not in name:
+        pytest.skip(f"variant not instantiated for {shape} ({name})")
+    C, C_ref, _ = parity(m, k, n, N, M, V, "int", seed=11 + m + n)
+    assert bool(np.array_equal(C.astype(np.float64), C_ref)), \
+        f"{name}: {int(np.count_nonzero(C.astype(np.float64) != C_ref))} outputs differ"
