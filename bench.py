@@ -42,12 +42,28 @@ CACHE_BYTES = 288 << 20      # 256 MB Infinity Cache + 8 x 4 MB L2
 # WRITE_SIZE (KiB per dispatch), each scaled by the factor the same counter
 # reads for a copy kernel of known size.  Valid only for the kernel source
 # hash it was taken on; null otherwise.
-TRAFFIC = {}
+TRAFFIC = {
+    ("R2", "482f352952bc28ba"): {
+        "fetch_kib": 132237.2, "fetch_factor": 1.99995,
+        "write_kib": 65536.0, "write_factor": 1.0,
+    },
+}
+
+
+def traffic_bytes(entry):
+    """Calibrated read + write bytes per launch from one TRAFFIC entry."""
+    return 1024.0 * (entry["fetch_kib"] * entry["fetch_factor"] + entry["write_kib"] * entry["write_factor"])
 
 
 def kernel_source_sha():
-    p = os.path.join(ROOT, "paper_2503_01253_amd", "csrc", "nmspmm_kernels.hip")
-    return hashlib.sha256(open(p, "rb").read()).hexdigest()[:16]
+    """Hash of every device and dispatch source (a change invalidates TRAFFIC)."""
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2503_01253_amd", "csrc")
+    for name in sorted(os.listdir(csrc)):
+        if name.endswith((".hip", ".h", ".cpp")):
+            h.update(name.encode())
+            h.update(open(os.path.join(csrc, name), "rb").read())
+    return h.hexdigest()[:16]
 
 
 def log(msg):
@@ -120,6 +136,44 @@ def time_launches(torch, fn, steps, warmup):
     return t0.elapsed_time(t1), per
 
 
+def pct(xs, q):
+    xs = sorted(xs)
+    return xs[min(len(xs) - 1, max(0, int(round(q * (len(xs) - 1)))))]
+
+
+def time_graph(torch, launch, copies, batches, reps):
+    """Per-launch time from replays of a HIP graph that holds one launch per
+    operand copy (no host launch overhead between kernels): `batches` timed
+    batches of `reps` replays each; returns per-launch ms for every batch."""
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        for i in range(min(3, copies)):
+            launch(i, s.cuda_stream)
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        h = torch.cuda.current_stream().cuda_stream
+        for i in range(copies):
+            launch(i, h)
+    for _ in range(3):
+        g.replay()
+    torch.cuda.synchronize()
+    out = []
+    for _ in range(batches):
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            g.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        out.append(e0.elapsed_time(e1) / (reps * copies))
+    del g
+    return out
+
+
 def cpu_baseline(run, A, Bp, target_s):
     """The fp64 CPU oracle on the same workload, timed on the host cores."""
     import oracle
@@ -147,7 +201,11 @@ def cpu_baseline(run, A, Bp, target_s):
     }
 
 
-def measure(torch, nm, run, steps, warmup, with_dense):
+def measure(torch, nm, run, steps, warmup, with_dense, graph=False):
+    """Time one workload.  Per-launch HIP events on the launch stream for
+    launches long enough that host overhead hides behind them; for the
+    microsecond-scale ones (graph=True) replays of a captured HIP graph, so
+    the figure is the kernels' own time.  Reports median, p10 and p90."""
     w = Workload(run, torch, nm, with_dense=with_dense)
     handle = torch.cuda.current_stream().cuda_stream
     total_ms, per = time_launches(torch, lambda i: w.launch(i, handle), steps, warmup)
@@ -155,23 +213,46 @@ def measure(torch, nm, run, steps, warmup, with_dense):
         "workload": run.name, "m": run.m, "n": run.n, "k": run.k, "N": run.N, "M": run.M,
         "V": run.V, "kernel": nm.nmspmm_kernel_name(run.m, run.n, run.k, run.N, run.M, run.V),
         "copies": w.copies, "ms_per_step": total_ms / steps,
-        "kernel_ms_mean": statistics.fmean(per), "kernel_ms_median": statistics.median(per),
+        "kernel_ms_mean": statistics.fmean(per), "timing": "per-launch events",
     }
+    if graph:
+        per = time_graph(torch, w.launch, w.copies, 7, max(1, 200 // w.copies))
+        res["timing"] = "graph replay"
+        res["kernel_ms_mean"] = statistics.fmean(per)
+    res["kernel_ms_median"] = statistics.median(per)
+    res["kernel_ms_p10"] = pct(per, 0.1)
+    res["kernel_ms_p90"] = pct(per, 0.9)
     res["eff_tflops"] = run.useful_flops / (res["kernel_ms_median"] * 1e-3) / 1e12
     res["hbm_gbs_alg"] = run.alg_bytes / (res["kernel_ms_median"] * 1e-3) / 1e9
     ai = run.useful_flops / run.alg_bytes
     roof = min(PEAK_FP32_TFLOPS, ai * PEAK_HBM_GBS / 1e3)
     res["roof_tflops"] = roof
     res["roof_frac"] = res["eff_tflops"] / roof
-    res["bound"] = "hbm" if ai * PEAK_HBM_GBS / 1e3 < PEAK_FP32_TFLOPS else "fp32"
+    res["bound"] = "hbm" if ai * PEAK_HBM_GBS / 1e3 < PEAK_FP32_TFLOPS else "mfma"
     if with_dense:
-        d_total, d_per = time_launches(torch, w.launch_dense, max(10, steps // 4), 3)
+        if graph:
+            d_per = time_graph(torch, lambda i, h: w.launch_dense(i), w.copies, 5,
+                               max(1, 100 // w.copies))
+        else:
+            _, d_per = time_launches(torch, lambda i: w.launch_dense(i), max(10, steps // 4), 3)
         d_ms = statistics.median(d_per)
         res["dense_matmul_ms"] = d_ms
         res["speedup_vs_dense"] = d_ms / res["kernel_ms_median"]
         res["ideal_speedup"] = run.M / run.N
     w.free()
     return res, w
+
+
+def device_clocks():
+    """Current clocks as rocm-smi reports them (None where it is unavailable)."""
+    import subprocess
+    try:
+        out = subprocess.run(["rocm-smi", "--showclocks"], capture_output=True, text=True,
+                             timeout=20).stdout
+    except (OSError, subprocess.SubprocessError):
+        return None
+    lines = [ln.strip() for ln in out.splitlines() if "clk" in ln.lower() and "Mhz" in ln]
+    return lines[:8] or None
 
 
 def main():
@@ -183,6 +264,10 @@ def main():
     ap.add_argument("--no-sweep", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--launches-only", type=int, default=0, metavar="L",
+                    help="run L untimed launches of the workload and exit (for counter passes)")
+    ap.add_argument("--copy-only", type=int, default=0, metavar="L",
+                    help="run L plain 1 GiB device copies and exit (calibrates the HBM counters)")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -200,17 +285,37 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
 
     run = RUNS[args.workload]
+    if args.copy_only:
+        src = torch.empty(1 << 28, dtype=torch.float32, device="cuda").fill_(1.0)
+        dst = torch.empty_like(src)
+        for _ in range(args.copy_only):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"[bench] {args.copy_only} copies of {src.numel() * 4} bytes done")
+        return
+    if args.launches_only:
+        w = Workload(run, torch, nm)
+        handle = torch.cuda.current_stream().cuda_stream
+        for i in range(args.launches_only):
+            w.launch(i, handle)
+        torch.cuda.synchronize()
+        log(f"[bench] {args.launches_only} launches of {run.name} "
+            f"({nm.nmspmm_kernel_name(run.m, run.n, run.k, run.N, run.M, run.V)}) done")
+        return
     log(f"[bench] headline {run.describe()} steps={args.steps} warmup={args.warmup}")
-    head, w = measure(torch, nm, run, args.steps, args.warmup, with_dense=True)
+    head, w = measure(torch, nm, run, args.steps, args.warmup, with_dense=True, graph=run.m <= 256)
     log(f"[bench] {json.dumps(head)}")
 
     achieved = run.useful_flops / (head["kernel_ms_mean"] * 1e-3) / 1e12
     sha = kernel_source_sha()
     tr = TRAFFIC.get((run.name, sha))
+    tr = traffic_bytes(tr) if tr else None
     roofline = {
         "bound": "mfma", "achieved": achieved, "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s",
         "frac": achieved / PEAK_FP32_TFLOPS, "traffic": tr,
+        "traffic_unit": "bytes per launch, rocprofv3 FETCH_SIZE + WRITE_SIZE scaled by a 1 GiB copy",
         "kernel": head["kernel"], "kernel_ms_mean": head["kernel_ms_mean"],
+        "kernel_ms_p10": head["kernel_ms_p10"], "kernel_ms_p90": head["kernel_ms_p90"],
         "flops_per_launch": run.useful_flops, "alg_bytes_per_launch": run.alg_bytes,
         "kernel_src_sha": sha,
     }
@@ -227,8 +332,8 @@ def main():
             if name == run.name:
                 continue
             r = RUNS[name]
-            steps = 200 if r.m <= 256 else 30
-            res, _ = measure(torch, nm, r, steps, 5, with_dense=True)
+            small = r.m <= 256
+            res, _ = measure(torch, nm, r, 200 if small else 30, 5, with_dense=True, graph=small)
             log(f"[bench] sweep {json.dumps(res)}")
             sweep.append({k: (round(v, 5) if isinstance(v, float) else v) for k, v in res.items()})
             torch.cuda.empty_cache()
@@ -257,6 +362,7 @@ def main():
                           "pct_of_fp32_peak_50_62.5_75_87.5": [96, 93, 95, 88]},
         "sweep": sweep,
         "device": torch.cuda.get_device_name(0),
+        "device_clocks": device_clocks(),
     }
     print(json.dumps(line), flush=True)
 

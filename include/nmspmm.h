@@ -17,8 +17,8 @@
  * with no M/N rescaling (a caller wanting Eq. 1's factor scales Bc).
  *
  * Every entry point is extern "C", returns a status code and never throws.
- * The library holds no global state besides per-device kernel attributes
- * and is safe to call from several host threads.
+ * The library holds no global state and is safe to call from several host
+ * threads.
  */
 #ifndef NMSPMM_H
 #define NMSPMM_H
@@ -82,7 +82,11 @@ NMSPMM_API nmspmm_status_t nmspmm_compress(const float *B_dense, int64_t k, int6
  * validates its arguments, enqueues the kernel(s) and returns; it allocates
  * nothing and does not synchronize.  Kernel faults surface at the caller's
  * next synchronization.  m == 0 or n == 0 returns NMSPMM_OK without a launch;
- * k == 0 writes zeros to C.  idx contents are not validated on the device
+ * k == 0 writes zeros to C.  Summation order: fp32 MFMA accumulation in an
+ * order fixed by the kernel variant; when the variant splits k across
+ * workgroups (the name from nmspmm_kernel_name ends in "+zero,splitS" with
+ * S > 1) the partial tiles are added to C with fp32 atomics, so the last
+ * bits of C may differ between runs.  idx contents are not validated on the device
  * (use nmspmm_validate_idx on the host); an offset >= M is clamped to M-1
  * so that every access stays inside A, and the result is then unspecified.
  * Errors: NMSPMM_ERR_INVALID_ARG (bad shape, null pointer with non-empty

@@ -249,3 +249,16 @@ def test_skinny_variants_exact(shape, splits, cols, qpw, monkeypatch):
     C, C_ref, _ = parity(m, k, n, N, M, V, "int", seed=11 + m + n)
     assert bool(np.array_equal(C.astype(np.float64), C_ref)), \
         f"{name}: {int(np.count_nonzero(C.astype(np.float64) != C_ref))} outputs differ"
+
+
+def test_dense_comparator_is_true_fp32():
+    """The benchmark's dense comparator (torch.matmul on the decompressed B,
+    TF32 off) meets the same bar, so it is a true fp32 GEMM."""
+    torch.backends.cuda.matmul.allow_tf32 = False
+    torch.set_float32_matmul_precision("highest")
+    m, k, n, N, M, V = 256, 2048, 512, 16, 32, 32
+    A, Bp, _ = make_inputs(m, k, n, N, M, V, 21)
+    Bc, idx = oracle.compress(Bp, N, M, V)
+    C = torch.matmul(to_dev(A), to_dev(Bp)).cpu().numpy()
+    r = oracle.check(C, oracle.spmm(A, Bc, idx, m, n, k, N, M, V), oracle.bound(A, Bc, idx, m, n, k, N, M, V))
+    assert r, r
