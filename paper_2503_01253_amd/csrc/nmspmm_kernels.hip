@@ -85,6 +85,10 @@ const TileInfo TILES[] = {
     {"128x512m32", 128, 512, 32, 8, launch_tiled_128x512m32, tiled_fits_128x512m32},
     {"128x128m32", 128, 128, 32, 2, launch_tiled_128x128m32, tiled_fits_128x128m32},
     {"64x512m32", 64, 512, 32, 8, launch_tiled_64x512m32, tiled_fits_64x512m32},
+    {"128x256", 128, 256, 16, 8, launch_tiled_128x256, tiled_fits_128x256},
+    {"256x128", 256, 128, 16, 8, launch_tiled_256x128, tiled_fits_256x128},
+    {"128x256m32", 128, 256, 32, 8, launch_tiled_128x256m32, tiled_fits_128x256m32},
+    {"64x1024m32", 64, 1024, 32, 8, launch_tiled_64x1024m32, tiled_fits_64x1024m32},
 };
 constexpr int NTILES = sizeof(TILES) / sizeof(TILES[0]);
 
@@ -134,25 +138,30 @@ bool tile_ok(const TileInfo &t, int BV, int KA, int NQ, int64_t k, int V)
     return (int64_t)t.BM * k * 4 < (int64_t(1) << 31);
 }
 
+// Accumulator floats per lane: tiles with at most 64 fit two workgroups per
+// CU when their stage is shallow, the others one.
+int acc_per_lane(const TileInfo &t) { return t.BM * t.BN / (64 * t.waves); }
+
 // Fraction of the workgroup slots a tile grid keeps busy over its waves of
 // workgroups (the last wave is usually partial), with slots = CUs x
 // workgroups per CU.
 double occupancy_of_grid(const TileInfo &t, int64_t m, int64_t n)
 {
     const int64_t tiles = ((m + t.BM - 1) / t.BM) * ((n + t.BN - 1) / t.BN);
-    const int64_t slots = 256 * (t.waves <= 4 ? 2 : 1);
+    const int64_t slots = 256 * (acc_per_lane(t) <= 64 ? 2 : 1);
     const int64_t rounds = (tiles + slots - 1) / slots;
     return (double)tiles / (double)(rounds * slots);
 }
 
 // Tile-shape preference by problem size, from sweeps on MI355X:
-//  * m <= 128: 16- and 64-row tiles with split-k, which keep enough
-//    workgroups in flight to stream Bc;
+//  * m <= 128 (when the streaming kernel does not apply): 16- and 64-row
+//    tiles with split-k, which keep enough workgroups in flight to stream Bc;
 //  * m or n below 1024: the 128 x 128 tile (enough tiles to fill the chip);
 //  * otherwise the 256 x 256 tile for dense-ish levels (N/M >= 1/2) and the
 //    128 x 512 tile with 32 x 32 MFMAs for the sparser ones, unless its grid
 //    would leave more than a quarter of the chip idle in the last wave, where
-//    the 128 x 128 tile quantises better.
+//    the 128 x 256 tile with 32 x 32 MFMAs (two workgroups per CU)
+//    quantises better.
 int preferences(int64_t m, int64_t n, int N, int M, const TileInfo **out)
 {
     int c = 0;
@@ -166,9 +175,7 @@ int preferences(int64_t m, int64_t n, int N, int M, const TileInfo **out)
         return c;
     }
     const char *big = 2 * N >= M ? "256x256" : "128x512m32";
-    const TileInfo *bt = tile_by_name(big), *st = tile_by_name("128x128");
-    if (occupancy_of_grid(*bt, m, n) < 0.75 && occupancy_of_grid(*st, m, n) > occupancy_of_grid(*bt, m, n))
-        add("128x128");
+    if (occupancy_of_grid(*tile_by_name(big), m, n) < 0.75) add("128x256m32");
     add(big);
     if (2 * N >= M) { add("128x512m32"); } else { add("256x256"); }
     add("128x512"); add("128x128");
@@ -244,12 +251,12 @@ Plan make_plan(const float *A, const float *Bc, const float *C, int64_t m, int64
     // per-stage Bc buffer offsets reach (padded rows) x n x 4 bytes < 32 x n x 4
     if ((int64_t)32 * n * 4 >= (int64_t(1) << 31)) return p;
 
-    // Stage depth for the eight-wave tiles: the smallest KA (a multiple of 32
-    // and of M) whose stage holds at least 16 compressed rows, so every stage
+    // Stage depth for the large tiles: the smallest KA (a multiple of 32 and
+    // of M) whose stage holds at least 16 compressed rows, so every stage
     // carries enough MFMA work to cover its fixed cost; deeper ones are tried
-    // if it does not fit.  The small tiles (four waves or fewer) instead take
-    // the shallowest stage, whose smaller LDS ring lets more workgroups share
-    // a CU.
+    // if it does not fit.  The tiles with few accumulators per lane instead
+    // take the shallowest stage, whose smaller LDS ring lets two workgroups
+    // share a CU.
     int ka_order[3], nka = 0;
     for (int KA : {32, 64, 128})
         if (KA % M == 0 && (KA / M) * N >= 16) ka_order[nka++] = KA;
@@ -277,7 +284,7 @@ Plan make_plan(const float *A, const float *Bc, const float *C, int64_t m, int64
         if (!cand[j]) continue;
         const int bv = bv_for(cand[j]->MI, V);
         if (bv == 0 || !aligned(C, 4 * bv)) continue;
-        const bool small = cand[j]->waves <= 4;
+        const bool small = acc_per_lane(*cand[j]) <= 64;
         const int *order = small ? ka_small : ka_order;
         for (int i = 0; i < (small ? nks : nka) && !tile; ++i) {
             const int nq = stage_nq(order[i], (order[i] / M) * N);

@@ -42,6 +42,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
+#include <type_traits>
 
 namespace nmspmm {
 
@@ -66,9 +67,11 @@ constexpr int LDS_CAPACITY = 160 * 1024;
 // 16 lanes per K index), 32 -> v_mfma_f32_32x32x2_f32 (K = 2, 32 lanes per
 // K index).  The 32 x 32 form issues half as many instructions for the same
 // work and keeps the matrix pipe busier; it needs V to be a multiple of 32.
-template <int BM_, int BN_, int WM_, int WN_, int MI_ = 16>
+// RING: LDS slots per workgroup (2: loads one stage ahead; 3: two stages
+// ahead, which needs a second set of A staging registers).
+template <int BM_, int BN_, int WM_, int WN_, int MI_ = 16, int RING_ = 2>
 struct TileCfg {
-    static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_, MI = MI_;
+    static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_, MI = MI_, RING = RING_;
     static constexpr int NW = (BM / WM) * (BN / WN);
     static constexpr int NT = NW * 64;
     static constexpr int KG = 64 / MI;                 // K per MFMA (compressed rows)
@@ -91,6 +94,9 @@ struct Shape {
     static constexpr int B_FLOATS = RST * T::BN;
     static constexpr int X_INTS = T::NT;
     static constexpr int SLOT_BYTES = 4 * (A_FLOATS + B_FLOATS + X_INTS);
+    // LDS slots: the tile's ring depth when it fits, else two
+    static constexpr int NSLOT = T::RING == 3 && 3 * SLOT_BYTES <= LDS_CAPACITY ? 3 : 2;
+    static constexpr int LOOKAHEAD = NSLOT - 1;
     // A: 32 x 32 chunks, one per wave at a time, each thread a 4 x 4 block
     static constexpr int A_CHUNKS = ((T::BM + 31) / 32) * (KA / 32);
     static constexpr int ACH = (A_CHUNKS + T::NW - 1) / T::NW;
@@ -98,7 +104,7 @@ struct Shape {
     static constexpr int B_LANE = B_FLOATS * 4 / T::NT;
     static constexpr int B_W = B_LANE % 16 == 0 ? 16 : 4;
     static constexpr int B_CNT = B_LANE / B_W;
-    static constexpr bool FITS = 2 * SLOT_BYTES <= LDS_CAPACITY && KA % 32 == 0 &&
+    static constexpr bool FITS = NSLOT * SLOT_BYTES <= LDS_CAPACITY && KA % 32 == 0 &&
                                  T::WN % CG == 0 && RST * QBMAX <= T::NT &&
                                  (B_FLOATS * 4) % T::NT == 0 && B_LANE % 4 == 0 && B_CNT >= 1;
 };
@@ -165,14 +171,16 @@ __device__ __forceinline__ void lds_dma(__amdgpu_buffer_rsrc_t rsrc, void *dst, 
         __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void *)dst, 1, (int)off, 0, 0, 0);
 }
 
-// Workgroup barrier after this wave's outstanding global loads and DMA have
-// completed (vmcnt(0)) and its LDS accesses have too (lgkmcnt(0)).  No memory
-// fence beyond that is needed; the empty asm statements keep the compiler
-// from moving memory accesses across it.
+// Workgroup barrier after all but the last VM global loads / DMA of this
+// wave have completed (vmcnt(VM), VM < 64) and its LDS accesses have too
+// (lgkmcnt(0)).  No memory fence beyond that is needed; the empty asm
+// statements keep the compiler from moving memory accesses across it.
+template <int VM>
 __device__ __forceinline__ void stage_sync()
 {
+    static_assert(VM >= 0 && VM < 64, "vmcnt range");
     asm volatile("" ::: "memory");
-    __builtin_amdgcn_s_waitcnt(0 | (7 << 4) | (0 << 8) | (0 << 14));  // vmcnt(0) lgkmcnt(0)
+    __builtin_amdgcn_s_waitcnt((VM & 15) | (7 << 4) | (0 << 8) | ((VM >> 4) << 14));
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
 }
@@ -187,7 +195,8 @@ __global__ __launch_bounds__(T::NT) void nm_tiled_kernel(TiledArgs p)
     typedef typename vec_of<BV>::type bvec;
     typedef typename vec_of<RPL>::type avec;
 
-    __shared__ __align__(16) unsigned char lds[2 * S::SLOT_BYTES];
+    constexpr int NSLOT = S::NSLOT, LA = S::LOOKAHEAD;
+    __shared__ __align__(16) unsigned char lds[NSLOT * S::SLOT_BYTES];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     int tm, tn, split;
@@ -217,8 +226,10 @@ __global__ __launch_bounds__(T::NT) void nm_tiled_kernel(TiledArgs p)
     const int rows_valid = (int)min<int64_t>(BM, m - row0);
     const __amdgpu_buffer_rsrc_t a_rsrc =
         make_rsrc(p.A + row0 * k, (uint32_t)((int64_t)rows_valid * k * 4));
-    f32x4 ra[ACH][4];
-    auto load_a = [&](int s) {
+    f32x4 ra[LA][ACH][4];   // one register set per stage in flight
+    // `valid` false: the loads are still issued (so that every stage issues
+    // the same number of memory instructions) but read zeros
+    auto load_a = [&](int s, int set, bool valid) {
         const int64_t kc0 = (int64_t)s * KA;
 #pragma unroll
         for (int ch = 0; ch < ACH; ++ch) {
@@ -228,14 +239,14 @@ __global__ __launch_bounds__(T::NT) void nm_tiled_kernel(TiledArgs p)
 #pragma unroll
             for (int t = 0; t < 4; ++t) {
                 const int r = rbase + 4 * r8 + t;
-                const bool ok = chunk < S::A_CHUNKS && r < BM && kcol < k;
+                const bool ok = valid && chunk < S::A_CHUNKS && r < BM && kcol < k;
                 const uint32_t off = ok ? (uint32_t)((r * k + kcol) * 4) : OOB;
                 // the buffer load returns raw dwords; reinterpret them as floats
-                ra[ch][t] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(a_rsrc, (int)off, 0, 0));
+                ra[set][ch][t] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(a_rsrc, (int)off, 0, 0));
             }
         }
     };
-    auto store_a = [&](int slot) {
+    auto store_a = [&](int set, int slot) {
         float *As = reinterpret_cast<float *>(lds + slot * S::SLOT_BYTES);
 #pragma unroll
         for (int ch = 0; ch < ACH; ++ch) {
@@ -244,7 +255,8 @@ __global__ __launch_bounds__(T::NT) void nm_tiled_kernel(TiledArgs p)
             if (chunk < S::A_CHUNKS && rbase + 4 * r8 < BM) {
 #pragma unroll
                 for (int c = 0; c < 4; ++c) {
-                    const f32x4 v = {ra[ch][0][c], ra[ch][1][c], ra[ch][2][c], ra[ch][3][c]};
+                    const f32x4 v = {ra[set][ch][0][c], ra[set][ch][1][c], ra[set][ch][2][c],
+                                     ra[set][ch][3][c]};
                     *reinterpret_cast<f32x4 *>(As + (cbase + 4 * c8 + c) * AST + rbase + 4 * r8) = v;
                 }
             }
@@ -264,10 +276,10 @@ __global__ __launch_bounds__(T::NT) void nm_tiled_kernel(TiledArgs p)
     const int x_ul = tid / QB, x_bl = tid % QB;
     const bool x_ok = tid < RST * QB && x_ul < RS && b_first + x_bl < q;
     const uint32_t x_off = (uint32_t)(x_ul * q + b_first + x_bl);
-    auto dma_bx = [&](int s, int slot) {
+    auto dma_bx = [&](int s, int slot, bool valid) {
         unsigned char *bs = lds + slot * S::SLOT_BYTES + 4 * S::A_FLOATS;
         const int64_t u0 = (int64_t)s * RS;
-        const int64_t rows_left = min<int64_t>(RS, w - u0);
+        const int64_t rows_left = valid ? max<int64_t>(0, min<int64_t>(RS, w - u0)) : 0;
         const __amdgpu_buffer_rsrc_t b_rsrc = make_rsrc(p.Bc + u0 * n, (uint32_t)(rows_left * n * 4));
 #pragma unroll
         for (int i = 0; i < S::B_CNT; ++i)
@@ -352,20 +364,38 @@ __global__ __launch_bounds__(T::NT) void nm_tiled_kernel(TiledArgs p)
                     }
     };
 
-    // ---- double-buffered stages, one barrier each ----
+    // ---- stages in a ring of NSLOT LDS slots, one barrier each ----
+    // Stage i lives in slot i % NSLOT and its A registers in set i % LA.  Its
+    // loads are issued LA stages ahead; at the end of stage i-1 its A
+    // registers go to LDS, and the barrier that follows waits for every load
+    // except the LA-1 stages issued after it (VM_STAGE memory instructions
+    // each: A loads, Bc DMA, idx DMA).
+    constexpr int VM_STAGE = 4 * ACH + S::B_CNT + 1;
+    static_assert(VM_STAGE * (LA - 1) < 64, "vmcnt range");
+    // Every stage issues its VM_STAGE loads and its A store unconditionally
+    // (loads past the last stage read zeros), so the compiler's wait counts
+    // see one straight-line pattern and keep LA-1 stages of loads in flight
+    // across the barrier.  Register-set indices are compile-time constants
+    // (no indexed register moves): the loop is unrolled by LA, and when the
+    // stage count is not a multiple of LA a last phantom stage multiplies
+    // zeros.
     if (nst > 0) {
-        load_a(s_begin);
-        dma_bx(s_begin, 0);
-        store_a(0);
-        stage_sync();
-    }
-    for (int it = 0; it < nst; ++it) {
-        const int cur = it & 1;
-        const bool next = it + 1 < nst;
-        if (next) {
-            load_a(s_begin + it + 1);
-            dma_bx(s_begin + it + 1, cur ^ 1);
+        load_a(s_begin, 0, true);
+        dma_bx(s_begin, 0, true);
+        if constexpr (LA > 1) {
+            load_a(s_begin + 1, 1, nst > 1);
+            dma_bx(s_begin + 1, 1, nst > 1);
         }
+        store_a(0, 0);
+        stage_sync<VM_STAGE * (LA - 1)>();
+    }
+
+    // one stage; SET = it % LA
+    auto stage = [&](int it, auto set_tag) {
+        constexpr int SET = decltype(set_tag)::value;
+        const int cur = it % NSLOT;
+        load_a(s_begin + it + LA, SET, it + LA < nst);
+        dma_bx(s_begin + it + LA, (it + LA) % NSLOT, it + LA < nst);
         prep_offsets(cur);
         fetch(cur, 0, 0);
 #pragma unroll
@@ -377,9 +407,15 @@ __global__ __launch_bounds__(T::NT) void nm_tiled_kernel(TiledArgs p)
             mma(sl);
             __builtin_amdgcn_sched_barrier(0);
         }
-        if (next) store_a(cur ^ 1);
-        stage_sync();
+        store_a((SET + 1) % LA, (it + 1) % NSLOT);
+        stage_sync<VM_STAGE * (LA - 1)>();
+    };
+    for (int it = 0; it < nst; it += LA) {
+        stage(it, std::integral_constant<int, 0>{});
+        if constexpr (LA > 1) stage(it + 1, std::integral_constant<int, 1>{});
     }
+    // no load may still be writing LDS when the workgroup ends
+    __builtin_amdgcn_s_waitcnt(0 | (7 << 4) | (15 << 8) | (0 << 14));   // vmcnt(0)
 
     // ---- epilogue.  16x16x4: element e of lane l is row 4*(l/16)+e of the
     // MFMA tile; 32x32x2: row 8*(e/4) + 4*(l/32) + e%4.  The MFMA tile row i

@@ -21,6 +21,10 @@ NMSPMM_DECLARE_TILE(256x256m32)
 NMSPMM_DECLARE_TILE(128x512m32)
 NMSPMM_DECLARE_TILE(128x128m32)
 NMSPMM_DECLARE_TILE(64x512m32)
+NMSPMM_DECLARE_TILE(128x256)
+NMSPMM_DECLARE_TILE(256x128)
+NMSPMM_DECLARE_TILE(128x256m32)
+NMSPMM_DECLARE_TILE(64x1024m32)
 
 #undef NMSPMM_DECLARE_TILE
 

@@ -198,8 +198,9 @@ def test_out_of_range_offsets_stay_in_bounds():
     assert np.isfinite(C).all()
 
 
-TILES = ["256x256", "128x512", "128x128", "64x512", "16x512",
-         "256x256m32", "128x512m32", "128x128m32", "64x512m32", "skinny"]
+TILES = ["256x256", "128x512", "128x128", "64x512", "16x512", "128x256", "256x128",
+         "256x256m32", "128x512m32", "128x128m32", "64x512m32", "128x256m32", "64x1024m32",
+         "skinny"]
 FORCED = [
     (300, 256, 1088, 8, 32, 32),
     (130, 384, 1024, 4, 32, 64),
