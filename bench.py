@@ -32,7 +32,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
-from nm_workloads import RUNS, make_run  # noqa: E402
+from nm_workloads import RUNS, make_run, table_runs  # noqa: E402
 
 PEAK_FP32_TFLOPS = 157.3     # MI355X dense fp32 (vector = matrix), AMD spec
 PEAK_HBM_GBS = 8000.0        # MI355X HBM3E, AMD spec
@@ -40,11 +40,11 @@ CACHE_BYTES = 288 << 20      # 256 MB Infinity Cache + 8 x 4 MB L2
 
 # HBM traffic of the headline kernel from rocprofv3 --pmc FETCH_SIZE and
 # WRITE_SIZE (KiB per dispatch), each scaled by the factor the same counter
-# reads for a copy kernel of known size.  Valid only for the kernel source
-# hash it was taken on; null otherwise.
+# reads for a copy kernel of known size.  Keyed by workload, kernel variant
+# and the hash of that variant's device sources: null once any differs.
 TRAFFIC = {
-    ("R2", "482f352952bc28ba"): {
-        "fetch_kib": 132237.2, "fetch_factor": 1.99995,
+    ("R2", "nm_tiled_kernel<256x256,bv2,ka32,nq4>,split1", "414b64ea4482fd16"): {
+        "fetch_kib": 132238.8, "fetch_factor": 1.99995,
         "write_kib": 65536.0, "write_factor": 1.0,
     },
 }
@@ -55,14 +55,22 @@ def traffic_bytes(entry):
     return 1024.0 * (entry["fetch_kib"] * entry["fetch_factor"] + entry["write_kib"] * entry["write_factor"])
 
 
-def kernel_source_sha():
-    """Hash of every device and dispatch source (a change invalidates TRAFFIC)."""
-    h = hashlib.sha256()
+def kernel_source_sha(kernel_name):
+    """Hash of the device sources of the named kernel variant: the tiled
+    kernel's header plus its tile's instantiation unit, or the streaming
+    kernel's file (a change invalidates TRAFFIC)."""
     csrc = os.path.join(ROOT, "paper_2503_01253_amd", "csrc")
-    for name in sorted(os.listdir(csrc)):
-        if name.endswith((".hip", ".h", ".cpp")):
-            h.update(name.encode())
-            h.update(open(os.path.join(csrc, name), "rb").read())
+    files = ["nmspmm_tiled.h"]
+    if kernel_name.startswith("nm_tiled_kernel<"):
+        files.append(f"nmspmm_tiled_{kernel_name.split('<')[1].split(',')[0]}.hip")
+    elif kernel_name.startswith("nm_skinny_kernel<"):
+        files.append("nmspmm_skinny.hip")
+    else:
+        files.append("nmspmm_kernels.hip")
+    h = hashlib.sha256()
+    for name in files:
+        h.update(name.encode())
+        h.update(open(os.path.join(csrc, name), "rb").read())
     return h.hexdigest()[:16]
 
 
@@ -263,6 +271,8 @@ def main():
     ap.add_argument("--workload", default="R2", choices=sorted(RUNS))
     ap.add_argument("--no-sweep", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-table", action="store_true",
+                    help="skip the shape x sparsity sweep (matrix-size table A-F x 0-87.5 %%)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--launches-only", type=int, default=0, metavar="L",
                     help="run L untimed launches of the workload and exit (for counter passes)")
@@ -307,8 +317,8 @@ def main():
     log(f"[bench] {json.dumps(head)}")
 
     achieved = run.useful_flops / (head["kernel_ms_mean"] * 1e-3) / 1e12
-    sha = kernel_source_sha()
-    tr = TRAFFIC.get((run.name, sha))
+    sha = kernel_source_sha(head["kernel"])
+    tr = TRAFFIC.get((run.name, head["kernel"], sha))
     tr = traffic_bytes(tr) if tr else None
     roofline = {
         "bound": "mfma", "achieved": achieved, "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s",
@@ -338,6 +348,32 @@ def main():
             sweep.append({k: (round(v, 5) if isinstance(v, float) else v) for k, v in res.items()})
             torch.cuda.empty_cache()
 
+    table = []
+    if not args.no_table:
+        dense_ms = {}
+        for name, r in table_runs().items():
+            shape = name.split("-")[0]
+            with_dense = shape not in dense_ms
+            res, _ = measure(torch, nm, r, 50, 5, with_dense=with_dense, graph=True)
+            if with_dense:
+                dense_ms[shape] = res["dense_matmul_ms"]
+            d = dense_ms[shape]
+            row = {
+                "point": name, "m": r.m, "n": r.n, "k": r.k, "N": r.N, "M": r.M, "V": r.V,
+                "sparsity_pct": round(100.0 * (1 - r.N / r.M), 1), "kernel": res["kernel"],
+                "us": round(res["kernel_ms_median"] * 1e3, 2),
+                "us_p10": round(res["kernel_ms_p10"] * 1e3, 2),
+                "us_p90": round(res["kernel_ms_p90"] * 1e3, 2),
+                "eff_tflops": round(res["eff_tflops"], 2),
+                "frac_fp32_peak": round(res["eff_tflops"] / PEAK_FP32_TFLOPS, 4),
+                "dense_fp32_us": round(d * 1e3, 2),
+                "speedup_vs_dense": round(d / res["kernel_ms_median"], 3),
+                "ideal_speedup": r.M / r.N,
+            }
+            log(f"[bench] table {json.dumps(row)}")
+            table.append(row)
+            torch.cuda.empty_cache()
+
     ms = head["ms_per_step"]
     line = {
         "metric": "effective TFLOPS (2*m*n*k*N/M)",
@@ -361,6 +397,7 @@ def main():
                           "workload": "m=n=k=4096, vector length not stated",
                           "pct_of_fp32_peak_50_62.5_75_87.5": [96, 93, 95, 88]},
         "sweep": sweep,
+        "shape_sparsity_table": table,
         "device": torch.cuda.get_device_name(0),
         "device_clocks": device_clocks(),
     }

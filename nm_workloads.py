@@ -78,6 +78,27 @@ RUNS = {
 }
 
 
+# The kernel-family sweep of Sec. IV-C: the six small / medium / large shapes
+# of the paper's matrix-size table (A-F) at the five sparsity levels of
+# Sec. IV-B and IV-C, 0 % (N = M = 32, the dense-equivalence point), 50 %,
+# 62.5 %, 75 % and 87.5 %; V = 32, U[-1, 1].
+TABLE_SHAPES = {
+    "A": (512, 512, 512), "B": (512, 1024, 1024), "C": (512, 2048, 2048),
+    "D": (1024, 2048, 2048), "E": (2048, 4096, 4096), "F": (4096, 4096, 4096),
+}
+TABLE_LEVELS = (32, 16, 12, 8, 4)    # N at M = 32
+
+
+def table_runs():
+    """Runs of the shape x sparsity sweep, keyed "A-32" .. "F-4" (shape-N)."""
+    out = {}
+    for i, (label, (m, n, k)) in enumerate(TABLE_SHAPES.items()):
+        for j, N in enumerate(TABLE_LEVELS):
+            name = f"{label}-{N}"
+            out[name] = Run(name, m, k, n, N, 32, 32, "uniform", 2000 + 10 * i + j)
+    return out
+
+
 def random_mask(rng: np.random.Generator, k: int, n: int, N: int, M: int, V: int) -> np.ndarray:
     """Boolean k x n mask: N kept rows per (window of M rows, block of V columns)."""
     G, q = k // M, n // V

@@ -156,7 +156,8 @@ double occupancy_of_grid(const TileInfo &t, int64_t m, int64_t n)
 // Tile-shape preference by problem size, from sweeps on MI355X:
 //  * m <= 128 (when the streaming kernel does not apply): 16- and 64-row
 //    tiles with split-k, which keep enough workgroups in flight to stream Bc;
-//  * m or n below 1024: the 128 x 128 tile (enough tiles to fill the chip);
+//  * m or n below 1024: the 128 x 256 tile with 32 x 32 MFMAs, else the
+//    128 x 128 tile (enough tiles to fill the chip, with split-k);
 //  * otherwise the 256 x 256 tile for dense-ish levels (N/M >= 1/2) and the
 //    128 x 512 tile with 32 x 32 MFMAs for the sparser ones, unless its grid
 //    would leave more than a quarter of the chip idle in the last wave, where
@@ -171,7 +172,7 @@ int preferences(int64_t m, int64_t n, int N, int M, const TileInfo **out)
         return c;
     }
     if (m < 1024 || n < 1024) {
-        add("128x128"); add("128x512"); add("256x256");
+        add("128x256m32"); add("128x128"); add("128x512"); add("256x256");
         return c;
     }
     const char *big = 2 * N >= M ? "256x256" : "128x512m32";
@@ -182,11 +183,16 @@ int preferences(int64_t m, int64_t n, int N, int M, const TileInfo **out)
     return c;
 }
 
-// Rows of C up to which the streaming kernel is used.  It re-reads Bc once
-// per 16 rows (mostly from L2 and the Infinity Cache), the tiled kernel once
-// per 128 or more; on MI355X the streaming kernel is faster up to 128 rows
-// at k = n = 8192.
-constexpr int64_t SKINNY_MAX_M = 128;
+// The streaming kernel re-reads Bc once per 16 rows of C (mostly from L2 and
+// the Infinity Cache), the tiled kernel once per 128 or more.  On MI355X the
+// streaming kernel is faster up to 128 rows at k = n = 8192, and on small
+// products (m * w below 2^19, e.g. 512 x 2048 x 2048 at 62.5 %), where the
+// tiled kernel's grid would be mostly split-k.
+bool prefer_streaming(int64_t m, int64_t k, int N, int M)
+{
+    const int64_t w = (k / M) * N;
+    return m <= 128 || (m <= 1024 && m * w < (int64_t(1) << 19));
+}
 
 int env_int(const char *name, int fallback)  // tuning sweeps only
 {
@@ -243,7 +249,8 @@ Plan make_plan(const float *A, const float *Bc, const float *C, int64_t m, int64
     Plan p;
     if (m == 0 || n == 0) return p;
     const char *force_tile = std::getenv("NMSPMM_TILE");  // tuning sweeps only
-    const bool want_skinny = force_tile ? std::strcmp(force_tile, "skinny") == 0 : m <= SKINNY_MAX_M;
+    const bool want_skinny =
+        force_tile ? std::strcmp(force_tile, "skinny") == 0 : prefer_streaming(m, k, N, M);
     if (want_skinny && plan_skinny(A, Bc, C, m, n, k, N, M, V, p)) return p;
     p.kind = Kind::General;
     if (k % 4 != 0 || V % 16 != 0 || 128 % M != 0) return p;
@@ -251,20 +258,21 @@ Plan make_plan(const float *A, const float *Bc, const float *C, int64_t m, int64
     // per-stage Bc buffer offsets reach (padded rows) x n x 4 bytes < 32 x n x 4
     if ((int64_t)32 * n * 4 >= (int64_t(1) << 31)) return p;
 
-    // Stage depth for the large tiles: the smallest KA (a multiple of 32 and
-    // of M) whose stage holds at least 16 compressed rows, so every stage
-    // carries enough MFMA work to cover its fixed cost; deeper ones are tried
-    // if it does not fit.  The tiles with few accumulators per lane instead
-    // take the shallowest stage, whose smaller LDS ring lets two workgroups
-    // share a CU.
-    int ka_order[3], nka = 0;
-    for (int KA : {32, 64, 128})
-        if (KA % M == 0 && (KA / M) * N >= 16) ka_order[nka++] = KA;
-    for (int KA : {128, 64, 32})
-        if (KA % M == 0 && (KA / M) * N < 16) ka_order[nka++] = KA;
-    int ka_small[3], nks = 0;
-    for (int KA : {32, 64, 128})
-        if (KA % M == 0) ka_small[nks++] = KA;
+    // Stage depth: the smallest KA (a multiple of 32 and of M) whose stage
+    // holds at least 16 compressed rows for the large tiles (8 for the tiles
+    // with few accumulators per lane, which share a CU between workgroups
+    // and prefer a small LDS ring), so every stage carries enough MFMA work
+    // to cover its fixed cost; deeper ones are tried if it does not fit.
+    auto ka_list = [&](int min_rows, int *order) {
+        int cnt = 0;
+        for (int KA : {32, 64, 128})
+            if (KA % M == 0 && (KA / M) * N >= min_rows) order[cnt++] = KA;
+        for (int KA : {128, 64, 32})
+            if (KA % M == 0 && (KA / M) * N < min_rows) order[cnt++] = KA;
+        return cnt;
+    };
+    int ka_order[3], ka_small[3];
+    int nka = ka_list(16, ka_order), nks = ka_list(8, ka_small);
     const int ka_force = env_int("NMSPMM_KA", 0);
     if (ka_force == 32 || ka_force == 64 || ka_force == 128) {
         ka_order[0] = ka_small[0] = ka_force;

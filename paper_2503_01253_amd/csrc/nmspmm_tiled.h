@@ -42,7 +42,6 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
-#include <type_traits>
 
 namespace nmspmm {
 
@@ -67,11 +66,9 @@ constexpr int LDS_CAPACITY = 160 * 1024;
 // 16 lanes per K index), 32 -> v_mfma_f32_32x32x2_f32 (K = 2, 32 lanes per
 // K index).  The 32 x 32 form issues half as many instructions for the same
 // work and keeps the matrix pipe busier; it needs V to be a multiple of 32.
-// RING: LDS slots per workgroup (2: loads one stage ahead; 3: two stages
-// ahead, which needs a second set of A staging registers).
-template <int BM_, int BN_, int WM_, int WN_, int MI_ = 16, int RING_ = 2>
+template <int BM_, int BN_, int WM_, int WN_, int MI_ = 16>
 struct TileCfg {
-    static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_, MI = MI_, RING = RING_;
+    static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_, MI = MI_;
     static constexpr int NW = (BM / WM) * (BN / WN);
     static constexpr int NT = NW * 64;
     static constexpr int KG = 64 / MI;                 // K per MFMA (compressed rows)
@@ -94,9 +91,11 @@ struct Shape {
     static constexpr int B_FLOATS = RST * T::BN;
     static constexpr int X_INTS = T::NT;
     static constexpr int SLOT_BYTES = 4 * (A_FLOATS + B_FLOATS + X_INTS);
-    // LDS slots: the tile's ring depth when it fits, else two
-    static constexpr int NSLOT = T::RING == 3 && 3 * SLOT_BYTES <= LDS_CAPACITY ? 3 : 2;
-    static constexpr int LOOKAHEAD = NSLOT - 1;
+    // LDS slots: two (the loads of stage s+1 are in flight while stage s is
+    // multiplied).  A three-slot ring with loads two stages ahead measured
+    // within 1-3 % on MI355X at the cost of a second set of A staging
+    // registers (and spills on the 128-accumulator tiles), so it is not used.
+    static constexpr int NSLOT = 2;
     // A: 32 x 32 chunks, one per wave at a time, each thread a 4 x 4 block
     static constexpr int A_CHUNKS = ((T::BM + 31) / 32) * (KA / 32);
     static constexpr int ACH = (A_CHUNKS + T::NW - 1) / T::NW;
@@ -171,16 +170,14 @@ __device__ __forceinline__ void lds_dma(__amdgpu_buffer_rsrc_t rsrc, void *dst, 
         __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void *)dst, 1, (int)off, 0, 0, 0);
 }
 
-// Workgroup barrier after all but the last VM global loads / DMA of this
-// wave have completed (vmcnt(VM), VM < 64) and its LDS accesses have too
-// (lgkmcnt(0)).  No memory fence beyond that is needed; the empty asm
-// statements keep the compiler from moving memory accesses across it.
-template <int VM>
+// Workgroup barrier after this wave's outstanding global loads and DMA have
+// completed (vmcnt(0)) and its LDS accesses have too (lgkmcnt(0)).  No memory
+// fence beyond that is needed; the empty asm statements keep the compiler
+// from moving memory accesses across it.
 __device__ __forceinline__ void stage_sync()
 {
-    static_assert(VM >= 0 && VM < 64, "vmcnt range");
     asm volatile("" ::: "memory");
-    __builtin_amdgcn_s_waitcnt((VM & 15) | (7 << 4) | (0 << 8) | ((VM >> 4) << 14));
+    __builtin_amdgcn_s_waitcnt(0 | (7 << 4) | (0 << 8) | (0 << 14));  // vmcnt(0) lgkmcnt(0)
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
 }
@@ -195,7 +192,7 @@ __global__ __launch_bounds__(T::NT) void nm_tiled_kernel(TiledArgs p)
     typedef typename vec_of<BV>::type bvec;
     typedef typename vec_of<RPL>::type avec;
 
-    constexpr int NSLOT = S::NSLOT, LA = S::LOOKAHEAD;
+    constexpr int NSLOT = S::NSLOT;
     __shared__ __align__(16) unsigned char lds[NSLOT * S::SLOT_BYTES];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -226,10 +223,10 @@ __global__ __launch_bounds__(T::NT) void nm_tiled_kernel(TiledArgs p)
     const int rows_valid = (int)min<int64_t>(BM, m - row0);
     const __amdgpu_buffer_rsrc_t a_rsrc =
         make_rsrc(p.A + row0 * k, (uint32_t)((int64_t)rows_valid * k * 4));
-    f32x4 ra[LA][ACH][4];   // one register set per stage in flight
+    f32x4 ra[ACH][4];
     // `valid` false: the loads are still issued (so that every stage issues
-    // the same number of memory instructions) but read zeros
-    auto load_a = [&](int s, int set, bool valid) {
+    // the same memory instructions) but read zeros
+    auto load_a = [&](int s, bool valid) {
         const int64_t kc0 = (int64_t)s * KA;
 #pragma unroll
         for (int ch = 0; ch < ACH; ++ch) {
@@ -242,11 +239,11 @@ __global__ __launch_bounds__(T::NT) void nm_tiled_kernel(TiledArgs p)
                 const bool ok = valid && chunk < S::A_CHUNKS && r < BM && kcol < k;
                 const uint32_t off = ok ? (uint32_t)((r * k + kcol) * 4) : OOB;
                 // the buffer load returns raw dwords; reinterpret them as floats
-                ra[set][ch][t] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(a_rsrc, (int)off, 0, 0));
+                ra[ch][t] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(a_rsrc, (int)off, 0, 0));
             }
         }
     };
-    auto store_a = [&](int set, int slot) {
+    auto store_a = [&](int slot) {
         float *As = reinterpret_cast<float *>(lds + slot * S::SLOT_BYTES);
 #pragma unroll
         for (int ch = 0; ch < ACH; ++ch) {
@@ -255,8 +252,7 @@ __global__ __launch_bounds__(T::NT) void nm_tiled_kernel(TiledArgs p)
             if (chunk < S::A_CHUNKS && rbase + 4 * r8 < BM) {
 #pragma unroll
                 for (int c = 0; c < 4; ++c) {
-                    const f32x4 v = {ra[set][ch][0][c], ra[set][ch][1][c], ra[set][ch][2][c],
-                                     ra[set][ch][3][c]};
+                    const f32x4 v = {ra[ch][0][c], ra[ch][1][c], ra[ch][2][c], ra[ch][3][c]};
                     *reinterpret_cast<f32x4 *>(As + (cbase + 4 * c8 + c) * AST + rbase + 4 * r8) = v;
                 }
             }
@@ -364,38 +360,24 @@ __global__ __launch_bounds__(T::NT) void nm_tiled_kernel(TiledArgs p)
                     }
     };
 
-    // ---- stages in a ring of NSLOT LDS slots, one barrier each ----
-    // Stage i lives in slot i % NSLOT and its A registers in set i % LA.  Its
-    // loads are issued LA stages ahead; at the end of stage i-1 its A
-    // registers go to LDS, and the barrier that follows waits for every load
-    // except the LA-1 stages issued after it (VM_STAGE memory instructions
-    // each: A loads, Bc DMA, idx DMA).
-    constexpr int VM_STAGE = 4 * ACH + S::B_CNT + 1;
-    static_assert(VM_STAGE * (LA - 1) < 64, "vmcnt range");
-    // Every stage issues its VM_STAGE loads and its A store unconditionally
-    // (loads past the last stage read zeros), so the compiler's wait counts
-    // see one straight-line pattern and keep LA-1 stages of loads in flight
-    // across the barrier.  Register-set indices are compile-time constants
-    // (no indexed register moves): the loop is unrolled by LA, and when the
-    // stage count is not a multiple of LA a last phantom stage multiplies
-    // zeros.
+    // ---- double-buffered stages, one barrier each ----
+    // Stage i lives in LDS slot i % 2.  Its loads are issued while stage i-1
+    // is multiplied; its A registers go to LDS at the end of stage i-1, and
+    // the barrier that follows waits for them and for its DMA.  Every stage
+    // issues its loads and its A store unconditionally (loads past the last
+    // stage read zeros), so the compiler's wait counts see one straight-line
+    // pattern.
     if (nst > 0) {
-        load_a(s_begin, 0, true);
+        load_a(s_begin, true);
         dma_bx(s_begin, 0, true);
-        if constexpr (LA > 1) {
-            load_a(s_begin + 1, 1, nst > 1);
-            dma_bx(s_begin + 1, 1, nst > 1);
-        }
-        store_a(0, 0);
-        stage_sync<VM_STAGE * (LA - 1)>();
+        store_a(0);
+        stage_sync();
     }
-
-    // one stage; SET = it % LA
-    auto stage = [&](int it, auto set_tag) {
-        constexpr int SET = decltype(set_tag)::value;
-        const int cur = it % NSLOT;
-        load_a(s_begin + it + LA, SET, it + LA < nst);
-        dma_bx(s_begin + it + LA, (it + LA) % NSLOT, it + LA < nst);
+    for (int it = 0; it < nst; ++it) {
+        const int cur = it & 1;
+        const bool next = it + 1 < nst;
+        load_a(s_begin + it + 1, next);
+        dma_bx(s_begin + it + 1, cur ^ 1, next);
         prep_offsets(cur);
         fetch(cur, 0, 0);
 #pragma unroll
@@ -407,15 +389,9 @@ __global__ __launch_bounds__(T::NT) void nm_tiled_kernel(TiledArgs p)
             mma(sl);
             __builtin_amdgcn_sched_barrier(0);
         }
-        store_a((SET + 1) % LA, (it + 1) % NSLOT);
-        stage_sync<VM_STAGE * (LA - 1)>();
-    };
-    for (int it = 0; it < nst; it += LA) {
-        stage(it, std::integral_constant<int, 0>{});
-        if constexpr (LA > 1) stage(it + 1, std::integral_constant<int, 1>{});
+        store_a(cur ^ 1);
+        stage_sync();
     }
-    // no load may still be writing LDS when the workgroup ends
-    __builtin_amdgcn_s_waitcnt(0 | (7 << 4) | (15 << 8) | (0 << 14));   // vmcnt(0)
 
     // ---- epilogue.  16x16x4: element e of lane l is row 4*(l/16)+e of the
     // MFMA tile; 32x32x2: row 8*(e/4) + 4*(l/32) + e%4.  The MFMA tile row i

@@ -10,7 +10,7 @@ import numpy as np
 import pytest
 
 import oracle
-from nm_workloads import RUNS, make_inputs, make_run
+from nm_workloads import RUNS, make_inputs, make_run, table_runs
 
 torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
@@ -130,6 +130,28 @@ def test_parity_full_size_sampled_rows(name):
     Bnd = oracle.bound(As, Bc_o, idx_o, len(rows), n, k, N, M, V)
     r = oracle.check(C[rows], C_ref, Bnd)
     say(f"[full] {name}: {r}")
+    assert r, r
+
+
+TABLE = table_runs()
+
+
+@pytest.mark.parametrize("name", list(TABLE))
+def test_shape_sparsity_table_sampled_rows(name):
+    """Every point of the shape x sparsity sweep (0 % to 87.5 %), in the launch
+    the benchmark times; the oracle computes a sample of rows."""
+    run = TABLE[name]
+    m, k, n, N, M, V = run.m, run.k, run.n, run.N, run.M, run.V
+    say(f"[table] {run.describe()} kernel={nm.nmspmm_kernel_name(m, n, k, N, M, V)}")
+    A, Bp, _ = make_run(run)
+    Bc, idx = nm.nmspmm_compress(Bp, N, M, V)
+    C = gpu_run(A, Bc, idx, m, n, k, N, M, V)
+    assert np.isfinite(C).all()
+    rng = np.random.default_rng(run.seed)
+    rows = np.array(sorted({0, m - 1, 127, 128, 255, 256} | set(int(x) for x in rng.integers(0, m, 6))))
+    As = np.ascontiguousarray(A[rows])
+    r = oracle.check(C[rows], oracle.spmm(As, Bc, idx, len(rows), n, k, N, M, V),
+                     oracle.bound(As, Bc, idx, len(rows), n, k, N, M, V))
     assert r, r
 
 
