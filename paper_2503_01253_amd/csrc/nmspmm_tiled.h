@@ -362,11 +362,13 @@ __global__ __launch_bounds__(T::NT) void nm_tiled_kernel(TiledArgs p)
 
     // ---- double-buffered stages, one barrier each ----
     // Stage i lives in LDS slot i % 2.  Its loads are issued while stage i-1
-    // is multiplied; its A registers go to LDS at the end of stage i-1, and
-    // the barrier that follows waits for them and for its DMA.  Every stage
-    // issues its loads and its A store unconditionally (loads past the last
-    // stage read zeros), so the compiler's wait counts see one straight-line
-    // pattern.
+    // is multiplied, after that stage's first MFMA K step: a wave whose
+    // memory instructions stall at issue then still has MFMAs in the pipe
+    // (issuing them before the first MFMA cost 5-12 % on MI355X).  Its A
+    // registers go to LDS at the end of stage i-1, and the barrier that
+    // follows waits for them and for its DMA.  Every stage issues its loads
+    // and its A store unconditionally (loads past the last stage read zeros),
+    // so the compiler's wait counts see one straight-line pattern.
     if (nst > 0) {
         load_a(s_begin, true);
         dma_bx(s_begin, 0, true);
@@ -376,8 +378,6 @@ __global__ __launch_bounds__(T::NT) void nm_tiled_kernel(TiledArgs p)
     for (int it = 0; it < nst; ++it) {
         const int cur = it & 1;
         const bool next = it + 1 < nst;
-        load_a(s_begin + it + 1, next);
-        dma_bx(s_begin + it + 1, cur ^ 1, next);
         prep_offsets(cur);
         fetch(cur, 0, 0);
 #pragma unroll
@@ -388,6 +388,10 @@ __global__ __launch_bounds__(T::NT) void nm_tiled_kernel(TiledArgs p)
             __builtin_amdgcn_sched_barrier(0);
             mma(sl);
             __builtin_amdgcn_sched_barrier(0);
+            if (ks == 0) {
+                load_a(s_begin + it + 1, next);
+                dma_bx(s_begin + it + 1, cur ^ 1, next);
+            }
         }
         store_a(cur ^ 1);
         stage_sync();
