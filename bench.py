@@ -120,11 +120,27 @@ class Workload:
         self.dense = None
 
 
-def time_launches(torch, fn, steps, warmup):
-    """Warm up, then time `steps` launches: total wall (events around the
-    whole batch) and per-launch durations (an event pair around each launch,
-    on the stream the kernel runs on)."""
+def warm_gpu(torch, fn, seconds):
+    """Launch `fn` until `seconds` of wall time have passed.  A cold MI355X
+    runs the first tens of milliseconds of work ~10 % slower (clock ramp), so
+    every timed batch is preceded by this much back-to-back work."""
+    t = time.perf_counter()
+    i = 0
+    while time.perf_counter() - t < seconds:
+        for _ in range(8):
+            fn(i)
+            i += 1
+        torch.cuda.synchronize()
+
+
+def time_launches(torch, fn, steps, warmup, warm_seconds=0.0):
+    """Warm up (`warmup` launches, after at least `warm_seconds` of work),
+    then time `steps` launches: total wall (events around the whole batch)
+    and per-launch durations (an event pair around each launch, on the
+    stream the kernel runs on)."""
     stream = torch.cuda.current_stream()
+    if warm_seconds > 0:
+        warm_gpu(torch, fn, warm_seconds)
     for i in range(warmup):
         fn(i)
     torch.cuda.synchronize()
@@ -165,9 +181,7 @@ def time_graph(torch, launch, copies, batches, reps):
         h = torch.cuda.current_stream().cuda_stream
         for i in range(copies):
             launch(i, h)
-    for _ in range(3):
-        g.replay()
-    torch.cuda.synchronize()
+    warm_gpu(torch, lambda i: g.replay(), 0.2)
     out = []
     for _ in range(batches):
         e0 = torch.cuda.Event(enable_timing=True)
@@ -209,14 +223,14 @@ def cpu_baseline(run, A, Bp, target_s):
     }
 
 
-def measure(torch, nm, run, steps, warmup, with_dense, graph=False):
+def measure(torch, nm, run, steps, warmup, with_dense, graph=False, warm_seconds=0.2):
     """Time one workload.  Per-launch HIP events on the launch stream for
     launches long enough that host overhead hides behind them; for the
     microsecond-scale ones (graph=True) replays of a captured HIP graph, so
     the figure is the kernels' own time.  Reports median, p10 and p90."""
     w = Workload(run, torch, nm, with_dense=with_dense)
     handle = torch.cuda.current_stream().cuda_stream
-    total_ms, per = time_launches(torch, lambda i: w.launch(i, handle), steps, warmup)
+    total_ms, per = time_launches(torch, lambda i: w.launch(i, handle), steps, warmup, warm_seconds)
     res = {
         "workload": run.name, "m": run.m, "n": run.n, "k": run.k, "N": run.N, "M": run.M,
         "V": run.V, "kernel": nm.nmspmm_kernel_name(run.m, run.n, run.k, run.N, run.M, run.V),
@@ -242,7 +256,7 @@ def measure(torch, nm, run, steps, warmup, with_dense, graph=False):
             d_per = time_graph(torch, lambda i, h: w.launch_dense(i), w.copies, 5,
                                max(1, 100 // w.copies))
         else:
-            _, d_per = time_launches(torch, lambda i: w.launch_dense(i), max(10, steps // 4), 3)
+            _, d_per = time_launches(torch, lambda i: w.launch_dense(i), max(10, steps // 4), 3, 0.2)
         d_ms = statistics.median(d_per)
         res["dense_matmul_ms"] = d_ms
         res["speedup_vs_dense"] = d_ms / res["kernel_ms_median"]
@@ -267,7 +281,7 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=100)
-    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=100)
     ap.add_argument("--workload", default="R2", choices=sorted(RUNS))
     ap.add_argument("--no-sweep", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
