@@ -6,14 +6,18 @@
 // windows of k (split-k across workgroups; the workgroups of one output tile
 // add into a zeroed C).  The slice is walked in chunks of at most SK_KC
 // columns of A:
-//   * the chunk of A (SK_ROWS x SK_KC, row-major, contiguous along k) is
-//     staged into LDS once, double-buffered, so that the gather of Eq. 1 reads
-//     LDS instead of scattering over L2 (the A_s tile of Sec. III-C);
-//   * its compressed rows are shared out to the NW waves in runs of QPW quads
-//     (4 compressed rows, the MFMA K).  A wave issues its Bc loads straight
-//     into MFMA operand registers (BV consecutive columns per lane), then the
-//     offset bytes of D for its rows and column blocks, then gathers A from
-//     LDS with those offsets and accumulates with v_mfma_f32_16x16x4_f32.
+//   * each chunk of A (SK_ROWS x SK_KC, row-major) arrives in LDS by
+//     buffer->LDS DMA, two chunks in flight in a two-buffer ring, so that
+//     the gather of Eq. 1 reads LDS instead of scattering over L2 (the A_s
+//     tile of Sec. III-C);
+//   * the chunk's compressed rows are shared out to the NW waves in rounds
+//     of QPW quads (4 compressed rows, the MFMA K) per wave.  A wave's Bc
+//     values go straight from global memory into MFMA operand registers (BV
+//     consecutive columns per lane) and its offset bytes of D into
+//     registers (the first round's loads are issued before the wait for
+//     the chunk's DMA, so the two latencies overlap).  The wave then gathers
+//     A from LDS with the offsets and accumulates with
+//     v_mfma_f32_16x16x4_f32.
 // Bc is read exactly once; no LDS staging is needed for it.  At the end the
 // waves' partial tiles are summed through LDS in a fixed order, so one
 // workgroup's contribution is deterministic; with split-k the workgroups'
@@ -32,17 +36,21 @@ namespace {
 constexpr int SK_ROWS = 16;     // rows of C per workgroup (one MFMA row tile)
 constexpr int SK_NW = 8;        // waves per workgroup
 constexpr int SK_NT = SK_NW * 64;
-constexpr int SK_KC = 1024;     // columns of A per staged chunk
-constexpr int SK_AS = SK_KC + 4;                  // LDS row stride of a staged chunk (floats)
+constexpr int SK_KC = 1024;     // columns of A per chunk
+constexpr int SK_AS = SK_KC + 4;                  // LDS row stride of a chunk (floats)
 constexpr int SK_ABUF = SK_ROWS * SK_AS;          // floats per chunk buffer
-constexpr int SK_A_LD = SK_ROWS * SK_KC / 4 / SK_NT;  // 16-byte A loads per thread and chunk
+constexpr int SK_SEG = 256;                       // floats per 16-byte DMA instruction (64 lanes)
+constexpr int SK_DMA = SK_ROWS * (SK_KC / SK_SEG) / SK_NW;   // DMA instructions per wave and chunk
+static_assert(SK_ROWS * (SK_KC / SK_SEG) % SK_NW == 0, "chunk DMA split");
 
-// Workgroup barrier that waits for this wave's LDS traffic only: global
-// loads issued for the next chunk stay in flight across it.
+// Workgroup barrier after all but the last VM global loads / DMA of this wave
+// have completed (vmcnt(VM), VM < 64) and its LDS accesses have too.
+template <int VM>
 __device__ __forceinline__ void lds_barrier()
 {
+    static_assert(VM >= 0 && VM < 64, "vmcnt range");
     asm volatile("" ::: "memory");
-    __builtin_amdgcn_s_waitcnt(0xF | (7 << 4) | (0 << 8) | (3 << 14));  // lgkmcnt(0)
+    __builtin_amdgcn_s_waitcnt((VM & 15) | (7 << 4) | (0 << 8) | ((VM >> 4) << 14));
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
 }
@@ -54,6 +62,8 @@ __global__ __launch_bounds__(SK_NT) void nm_skinny_kernel(SkinnyArgs p)
     constexpr int NG = COLS / CG;           // column groups per workgroup
     constexpr int RED = SK_NW * SK_ROWS * COLS;
     constexpr int LDS_FLOATS = 2 * SK_ABUF > RED ? 2 * SK_ABUF : RED;
+    constexpr int NL = 2 * QPW * NG;        // memory instructions per wave and round
+    static_assert(SK_DMA + NL < 64, "vmcnt range");
     typedef typename vec_of<BV>::type bvec;
 
     // two A chunk buffers during the main loop; the reduction area after it
@@ -84,27 +94,20 @@ __global__ __launch_bounds__(SK_NT) void nm_skinny_kernel(SkinnyArgs p)
     const __amdgpu_buffer_rsrc_t a_rsrc =
         make_rsrc(p.A + row0 * k, (uint32_t)((int64_t)rows_valid * k * 4));
 
-    // ---- A chunk staging: 16-byte loads along k, rows past m read as zero ----
-    f32x4 ra[SK_A_LD];
-    auto load_a = [&](int64_t c) {
+    // ---- A chunk c -> LDS buffer `buf` by DMA; rows past m and columns past
+    // the chunk read zero.  Issued unconditionally (valid false: all zeros)
+    // so that every wave issues the same memory instructions per chunk. ----
+    auto dma_a = [&](int64_t c, int buf, bool valid) {
         const int64_t g0 = gb + c * cw;
-        const int64_t kc0 = g0 * M, kcn = (min<int64_t>(ge, g0 + cw) - g0) * M;
+        const int64_t kc0 = g0 * M;
+        const int64_t kcn = valid ? (min<int64_t>(ge, g0 + cw) - g0) * M : 0;
 #pragma unroll
-        for (int i = 0; i < SK_A_LD; ++i) {
-            const int f = tid + SK_NT * i;
-            const int ar = f / (SK_KC / 4), c4 = f % (SK_KC / 4);
-            const bool ok = 4 * c4 < kcn;
-            const uint32_t off = ok ? (uint32_t)((ar * k + kc0 + 4 * c4) * 4) : OOB;
-            // the buffer load returns raw dwords; reinterpret them as floats
-            ra[i] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(a_rsrc, (int)off, 0, 0));
-        }
-    };
-    auto store_a = [&](int buf) {
-#pragma unroll
-        for (int i = 0; i < SK_A_LD; ++i) {
-            const int f = tid + SK_NT * i;
-            const int ar = f / (SK_KC / 4), c4 = f % (SK_KC / 4);
-            *reinterpret_cast<f32x4 *>(lds + buf * SK_ABUF + ar * SK_AS + 4 * c4) = ra[i];
+        for (int i = 0; i < SK_DMA; ++i) {
+            const int piece = wave * SK_DMA + i;
+            const int ar = piece / (SK_KC / SK_SEG), seg = piece % (SK_KC / SK_SEG);
+            const int col = seg * SK_SEG + 4 * lane;
+            const uint32_t off = col < kcn ? (uint32_t)((ar * k + kc0 + col) * 4) : OOB;
+            lds_dma<16>(a_rsrc, lds + buf * SK_ABUF + ar * SK_AS + seg * SK_SEG, off);
         }
     };
 
@@ -117,80 +120,102 @@ __global__ __launch_bounds__(SK_NT) void nm_skinny_kernel(SkinnyArgs p)
         gblk[g] = gcol[g] / V;
     }
 
+    // compressed rows [u0, u1) of chunk c and the first row of this wave's
+    // run in round rd
+    auto chunk_rows = [&](int64_t c, int64_t &u0, int64_t &u1) {
+        const int64_t w0 = gb + c * cw;
+        u0 = w0 * N;
+        u1 = min<int64_t>(ge, w0 + cw) * N;
+    };
+
+    // ---- one round's Bc operands and offsets, straight into registers ----
+    auto load_round = [&](int64_t c, int rd, bvec (&bv)[QPW][NG], int (&off)[QPW][NG]) {
+        int64_t u0, u1;
+        chunk_rows(c, u0, u1);
+        const int64_t ub = u0 + ((int64_t)rd * SK_NW + wave) * QPW * 4;
+#pragma unroll
+        for (int j = 0; j < QPW; ++j) {
+            const int64_t rows_left = max<int64_t>(0, u1 - (ub + 4 * j));
+            const __amdgpu_buffer_rsrc_t b_rsrc =
+                make_rsrc(p.Bc + (ub + 4 * j) * n,
+                          (uint32_t)(min<int64_t>(rows_left, 4) * n * 4));
+            const int64_t u = ub + 4 * j + kq;
+            const bool urow = u < u1;
+#pragma unroll
+            for (int g = 0; g < NG; ++g) {
+                const int64_t col = gcol[g] + BV * r;
+                const uint32_t boff = urow && col < n ? (uint32_t)((kq * n + col) * 4) : OOB;
+                // the buffer loads return raw dwords; reinterpret them as floats
+                if constexpr (BV == 4)
+                    bv[j][g] = __builtin_bit_cast(
+                        f32x4, __builtin_amdgcn_raw_buffer_load_b128(b_rsrc, (int)boff, 0, 0));
+                else if constexpr (BV == 2)
+                    bv[j][g] = __builtin_bit_cast(
+                        f32x2, __builtin_amdgcn_raw_buffer_load_b64(b_rsrc, (int)boff, 0, 0));
+                else
+                    bv[j][g] = __builtin_bit_cast(
+                        float, __builtin_amdgcn_raw_buffer_load_b32(b_rsrc, (int)boff, 0, 0));
+                const bool ok = urow && gcol[g] < n;
+                off[j][g] = p.idx[ok ? u * q + gblk[g] : 0];
+            }
+        }
+    };
+
     f32x4 acc[NG][BV];
 #pragma unroll
     for (int g = 0; g < NG; ++g)
 #pragma unroll
         for (int s = 0; s < BV; ++s) acc[g][s] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    if (nchunks > 0) {
-        load_a(0);
-        store_a(0);
-    }
-    for (int64_t c = 0; c < nchunks; ++c) {
-        const int buf = (int)(c & 1);
-        if (c + 1 < nchunks) load_a(c + 1);
-        // chunk c is in LDS; every wave is done with chunk c-1's buffer
-        lds_barrier();
-        const int64_t w0 = gb + c * cw;
-        const int64_t u0 = w0 * N, u1 = min<int64_t>(ge, w0 + cw) * N;
+    // ---- gather A from the chunk in `buf`, MFMAs ----
+    auto compute = [&](int buf, int64_t u0, int64_t u1, int rd, const bvec (&bv)[QPW][NG],
+                       const int (&off)[QPW][NG]) {
         const float *As = lds + buf * SK_ABUF + r * SK_AS;
-        for (int64_t ub = u0 + (int64_t)wave * QPW * 4; ub < u1; ub += (int64_t)SK_NW * QPW * 4) {
-            // 1. Bc, straight into operand registers (independent of D)
-            bvec bv[QPW][NG];
+        const int64_t ub = u0 + ((int64_t)rd * SK_NW + wave) * QPW * 4;
 #pragma unroll
-            for (int j = 0; j < QPW; ++j) {
-                const int64_t rows_left = max<int64_t>(0, u1 - (ub + 4 * j));
-                const __amdgpu_buffer_rsrc_t b_rsrc =
-                    make_rsrc(p.Bc + (ub + 4 * j) * n, (uint32_t)(min<int64_t>(rows_left, 4) * n * 4));
-                const bool urow = ub + 4 * j + kq < u1;
+        for (int j = 0; j < QPW; ++j) {
+            const int64_t u = ub + 4 * j + kq;
+            const int wbase = u < u1 ? (int)(((uint32_t)(u - u0) * invN) >> 20) * M : 0;
 #pragma unroll
-                for (int g = 0; g < NG; ++g) {
-                    const int64_t col = gcol[g] + BV * r;
-                    const uint32_t boff = urow && col < n ? (uint32_t)((kq * n + col) * 4) : OOB;
-                    // the buffer loads return raw dwords; reinterpret them as floats
-                    if constexpr (BV == 4)
-                        bv[j][g] = __builtin_bit_cast(
-                            f32x4, __builtin_amdgcn_raw_buffer_load_b128(b_rsrc, (int)boff, 0, 0));
-                    else if constexpr (BV == 2)
-                        bv[j][g] = __builtin_bit_cast(
-                            f32x2, __builtin_amdgcn_raw_buffer_load_b64(b_rsrc, (int)boff, 0, 0));
-                    else
-                        bv[j][g] = __builtin_bit_cast(
-                            float, __builtin_amdgcn_raw_buffer_load_b32(b_rsrc, (int)boff, 0, 0));
-                }
-            }
-            // 2. offsets of D for this lane's compressed row and each column block
-            int off[QPW][NG];
+            for (int g = 0; g < NG; ++g) {
+                const float a = As[wbase + min(off[j][g], M - 1)];
 #pragma unroll
-            for (int j = 0; j < QPW; ++j) {
-                const int64_t u = ub + 4 * j + kq;
-#pragma unroll
-                for (int g = 0; g < NG; ++g) {
-                    const bool ok = u < u1 && gcol[g] < n;
-                    off[j][g] = p.idx[ok ? u * q + gblk[g] : 0];
-                }
-            }
-            // 3. gather A from the staged chunk, MFMAs
-#pragma unroll
-            for (int j = 0; j < QPW; ++j) {
-                const int64_t u = ub + 4 * j + kq;
-                const int wbase = u < u1 ? (int)(((uint32_t)(u - u0) * invN) >> 20) * M : 0;
-#pragma unroll
-                for (int g = 0; g < NG; ++g) {
-                    const float a = As[wbase + min(off[j][g], M - 1)];
-#pragma unroll
-                    for (int s = 0; s < BV; ++s)
-                        acc[g][s] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, lane_of<BV>(bv[j][g], s),
-                                                                         acc[g][s], 0, 0, 0);
-                }
+                for (int s = 0; s < BV; ++s)
+                    acc[g][s] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, lane_of<BV>(bv[j][g], s),
+                                                                     acc[g][s], 0, 0, 0);
             }
         }
-        if (c + 1 < nchunks) store_a(buf ^ 1);
+    };
+
+    // ---- chunk loop.  Memory instructions in flight at the barrier that
+    // opens chunk c, newest first: the loads of round 0 of chunk c (NL), the
+    // DMA of chunk c+1 (SK_DMA); everything older, chunk c's DMA included,
+    // must be done.  (Loading round r+1 while round r is multiplied measured
+    // slower: the handover of the operand registers waits for the loads.) ----
+    bvec bv[QPW][NG];
+    int off[QPW][NG];
+    if (nchunks > 0) {
+        dma_a(0, 0, true);
+        dma_a(1, 1, nchunks > 1);
     }
+    for (int64_t c = 0; c < nchunks; ++c) {
+        int64_t u0, u1;
+        chunk_rows(c, u0, u1);
+        const int rounds = (int)((u1 - u0 + SK_NW * QPW * 4 - 1) / (SK_NW * QPW * 4));
+        load_round(c, 0, bv, off);
+        lds_barrier<SK_DMA + NL>();
+        for (int rd = 0; rd < rounds; ++rd) {
+            if (rd > 0) load_round(c, rd, bv, off);
+            compute((int)(c & 1), u0, u1, rd, bv, off);
+        }
+        // every wave is done with this buffer: refill it with chunk c+2
+        lds_barrier<63>();
+        dma_a(c + 2, (int)(c & 1), c + 2 < nchunks);
+    }
+    // no DMA may still be writing LDS when it becomes the reduction area
+    lds_barrier<0>();
 
     // ---- sum the waves' partial tiles through LDS (fixed order) ----
-    lds_barrier();   // every wave is done reading A chunks
     // lane l holds rows 4*(l/16)+e, columns g*CG + BV*(l%16)+s
     float *mine = lds + wave * SK_ROWS * COLS;
 #pragma unroll
@@ -206,7 +231,7 @@ __global__ __launch_bounds__(SK_NT) void nm_skinny_kernel(SkinnyArgs p)
             }
             *reinterpret_cast<bvec *>(mine + (4 * kq + e) * COLS + g * CG + BV * r) = v;
         }
-    lds_barrier();
+    lds_barrier<0>();
     // one output per lane and step, consecutive lanes on consecutive columns
     // (coalesced stores and atomics)
     constexpr int OUT = SK_ROWS * COLS;
@@ -240,12 +265,12 @@ int skinny_chunk_cols() { return SK_KC; }
 
 // Instantiated (BV, QPW, COLS): the ones that fit in registers without
 // spills, with BV * 16 <= COLS.
-#define NMSPMM_SKINNY_VARIANTS(X)                                       \
-    X(1, 1, 32) X(1, 2, 32) X(1, 4, 32) X(2, 1, 32) X(2, 2, 32) X(2, 4, 32) \
-    X(1, 1, 64) X(1, 2, 64) X(2, 1, 64) X(2, 2, 64) X(2, 4, 64)         \
-    X(4, 1, 64) X(4, 2, 64) X(4, 4, 64)                                 \
-    X(1, 1, 128) X(1, 2, 128) X(2, 1, 128) X(2, 2, 128) X(2, 4, 128)    \
-    X(4, 1, 128) X(4, 2, 128) X(4, 4, 128)                              \
+#define NMSPMM_SKINNY_VARIANTS(X)                                                    \
+    X(1, 1, 32) X(1, 2, 32) X(1, 4, 32) X(1, 8, 32) X(2, 1, 32) X(2, 2, 32) X(2, 4, 32) \
+    X(2, 8, 32) X(1, 1, 64) X(1, 2, 64) X(1, 4, 64) X(2, 1, 64) X(2, 2, 64) X(2, 4, 64) \
+    X(4, 1, 64) X(4, 2, 64) X(4, 4, 64) X(4, 8, 64)                                  \
+    X(1, 1, 128) X(1, 2, 128) X(2, 1, 128) X(2, 2, 128) X(2, 4, 128)                 \
+    X(4, 1, 128) X(4, 2, 128) X(4, 4, 128)                                           \
     X(1, 1, 256) X(2, 1, 256) X(2, 2, 256) X(4, 1, 256) X(4, 2, 256)
 
 bool skinny_has(int BV, int QPW, int COLS)

@@ -255,7 +255,8 @@ SKINNY = [
 
 
 @pytest.mark.parametrize("cols,qpw", [(256, 1), (256, 2), (128, 1), (128, 2), (128, 4),
-                                      (64, 1), (64, 2), (64, 4), (32, 1), (32, 2), (32, 4)])
+                                      (64, 1), (64, 2), (64, 4), (64, 8), (32, 1), (32, 2),
+                                      (32, 4), (32, 8)])
 @pytest.mark.parametrize("splits", [1, 3])
 @pytest.mark.parametrize("shape", SKINNY, ids=lambda s: "x".join(map(str, s)))
 def test_skinny_variants_exact(shape, splits, cols, qpw, monkeypatch):
