@@ -15,7 +15,7 @@ import numpy as np
 from .build import LIB_PATH, build
 
 __all__ = [
-    "build", "lib", "spmm", "bound", "compress", "decompress", "validate",
+    "build", "lib", "spmm", "bound", "compress", "decompress", "validate", "epilogue",
     "set_threads", "max_threads", "check", "CheckResult", "PARITY_RTOL",
 ]
 
@@ -45,6 +45,8 @@ def lib():
         L.oracle_validate.argtypes = [_U8, _I64, _I64, _I, _I, _I]
         L.oracle_shape_ok.argtypes = [_I64, _I64, _I64, _I, _I, _I]
         L.oracle_set_threads.argtypes = [_I]
+        L.oracle_epilogue.argtypes = [_D, _I64, _I64, ctypes.c_double, _F, _I]
+        L.oracle_epilogue.restype = _I
         for f in (L.oracle_spmm, L.oracle_bound, L.oracle_compress, L.oracle_decompress,
                   L.oracle_validate, L.oracle_shape_ok, L.oracle_max_threads):
             f.restype = _I
@@ -112,6 +114,24 @@ def validate(idx, k, n, N, M, V):
     """0 valid, 1 bad shape, 2 offset >= M, 3 not strictly increasing."""
     idx = _u8(idx)
     return int(lib().oracle_validate(_p(idx, _U8), k, n, N, M, V))
+
+
+ACTS = {"none": 0, "relu": 1, "gelu": 2}
+
+
+def epilogue(C, alpha=1.0, bias=None, act="none"):
+    """act(alpha * C + bias[j]) on an fp64 product (Eq. 1's M/N factor is
+    alpha = M/N); returns a new fp64 array."""
+    out = np.ascontiguousarray(C, dtype=np.float64).copy()
+    m, n = out.shape
+    b = None if bias is None else _f32(bias)
+    if b is not None and b.shape != (n,):
+        raise ValueError("bias must have n entries")
+    st = lib().oracle_epilogue(_p(out, _D), m, n, float(alpha),
+                               None if b is None else _p(b, _F), ACTS[act])
+    if st != 0:
+        raise ValueError(f"oracle_epilogue failed ({st})")
+    return out
 
 
 def set_threads(t: int) -> None:

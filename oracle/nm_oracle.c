@@ -221,3 +221,26 @@ int oracle_validate(const uint8_t *idx, int64_t k, int64_t n, int N, int M, int 
     }
     return 0;
 }
+
+/* Output epilogue, in place on an fp64 product C (m x n):
+ *   C[i][j] <- act(alpha * C[i][j] + bias[j])
+ * alpha = M/N applies Eq. 1's leading factor (Sec. II-A), which the product
+ * above leaves out.  The bias vector (n entries, may be NULL) and the
+ * activation are the usual epilogue of a linear layer such as the Llama
+ * layers of Sec. IV-A; the paper's operator itself has neither.
+ * act: 0 none; 1 ReLU, max(0, y); 2 GELU, y * Phi(y) with Phi the standard
+ * normal CDF, 0.5 * (1 + erf(y / sqrt(2))).  Returns 1 for an unknown act. */
+int oracle_epilogue(double *C, int64_t m, int64_t n, double alpha, const float *bias, int act)
+{
+    if (act < 0 || act > 2) return 1;
+    for (int64_t i = 0; i < m; ++i) {
+        for (int64_t j = 0; j < n; ++j) {
+            double y = alpha * C[i * n + j];
+            if (bias) y += (double)bias[j];
+            if (act == 1) y = y > 0.0 ? y : 0.0;
+            else if (act == 2) y = 0.5 * y * (1.0 + erf(y / sqrt(2.0)));
+            C[i * n + j] = y;
+        }
+    }
+    return 0;
+}

@@ -242,3 +242,23 @@ def test_checker_rejects_injected_errors():
     Bc2[5] = 0
     C2 = oracle.spmm(A, Bc2, idx, m, n, k, N, M, V)
     assert not oracle.check(C2, C, Bnd)
+
+
+def test_epilogue_pins():
+    """alpha, bias and activation against closed forms and scipy's normal CDF
+    (an independent implementation of Phi)."""
+    from scipy.stats import norm
+    rng = np.random.default_rng(5)
+    C = rng.standard_normal((7, 9)) * 3
+    bias = rng.standard_normal(9).astype(np.float32)
+    np.testing.assert_array_equal(oracle.epilogue(C), C)
+    np.testing.assert_array_equal(oracle.epilogue(C, alpha=4.0), 4.0 * C)   # Eq. 1's M/N at 8:32
+    np.testing.assert_array_equal(oracle.epilogue(C, bias=bias), C + bias.astype(np.float64))
+    np.testing.assert_array_equal(oracle.epilogue(C, act="relu"), np.maximum(C, 0.0))
+    y = 2.0 * C + bias.astype(np.float64)
+    np.testing.assert_allclose(oracle.epilogue(C, 2.0, bias, "gelu"), y * norm.cdf(y), rtol=1e-13, atol=1e-15)
+    g = oracle.epilogue(np.array([[0.0, 40.0, -40.0, 1.0]]), act="gelu")
+    assert g[0, 0] == 0.0 and g[0, 1] == 40.0 and g[0, 2] == 0.0
+    assert abs(g[0, 3] - 0.8413447460685429) < 1e-15          # Phi(1)
+    with pytest.raises(ValueError):
+        oracle.epilogue(C, bias=np.zeros(3, np.float32))

@@ -39,7 +39,12 @@ MUTANTS = {
     # compressor breaks ties toward the larger offset
     "ties_to_larger": ("if (best < 0 || score[o] > score[best]) best = o;",
                        "if (best < 0 || score[o] >= score[best]) best = o;"),
+    # epilogue: Eq. 1's factor dropped, GELU's argument unscaled, leaky ReLU
+    "alpha_dropped": ("double y = alpha * C[i * n + j];", "double y = C[i * n + j];"),
+    "gelu_scale": ("erf(y / sqrt(2.0))", "erf(y / 2.0)"),
+    "leaky_relu": ("y = y > 0.0 ? y : 0.0;", "y = y > 0.0 ? y : 0.01 * y;"),
 }
+EPILOGUE_MUTANTS = ("alpha_dropped", "gelu_scale", "leaky_relu")
 
 
 class _Lib:
@@ -51,7 +56,13 @@ class _Lib:
         I64, I = ctypes.c_int64, ctypes.c_int
         L.oracle_spmm.argtypes = [F, F, U8, D, I64, I64, I64, I, I, I]
         L.oracle_compress.argtypes = [F, I64, I64, I, I, I, F, U8]
+        L.oracle_epilogue.argtypes = [D, I64, I64, ctypes.c_double, F, I]
         self.L, self.F, self.D, self.U8 = L, F, D, U8
+
+    def epilogue(self, C, alpha, act):
+        out = np.ascontiguousarray(C, np.float64).copy()
+        self.L.oracle_epilogue(out.ctypes.data_as(self.D), out.shape[0], out.shape[1], alpha, None, act)
+        return out
 
     def compress(self, B, N, M, V):
         k, n = B.shape
@@ -118,6 +129,16 @@ def failing_pins(lib):
     _, idx = lib.compress(np.ones((8, 4), np.float32), 2, 4, 2)
     if not np.array_equal(idx, np.array([[0, 0], [1, 1], [0, 0], [1, 1]], np.uint8)):
         fails.append("ties")
+    # epilogue: alpha scales exactly, ReLU clamps at zero, GELU matches
+    # scipy's normal CDF
+    from scipy.stats import norm
+    C = np.linspace(-4, 4, 33)[None, :]
+    if not np.array_equal(lib.epilogue(C, 4.0, 0), 4.0 * C):
+        fails.append("epilogue_alpha")
+    if not np.array_equal(lib.epilogue(C, 1.0, 1), np.maximum(C, 0.0)):
+        fails.append("epilogue_relu")
+    if not np.allclose(lib.epilogue(C, 1.0, 2), C * norm.cdf(C), rtol=1e-13, atol=1e-15):
+        fails.append("epilogue_gelu")
     return fails
 
 
@@ -138,7 +159,7 @@ def test_every_planted_mistake_is_caught(tmp_path, source, name):
     # selection sites, in oracle_compress); only that one is changed
     at = source.find(old)
     assert at >= 0, f"mutation site for {name} not found"
-    if name not in ("keeps_smallest", "ties_to_larger"):
+    if name not in ("keeps_smallest", "ties_to_larger") + EPILOGUE_MUTANTS:
         assert at < source.index("int oracle_bound(")
     src = tmp_path / f"mutant_{name}.c"
     src.write_text(source.replace(old, new, 1))
