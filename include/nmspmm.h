@@ -96,6 +96,46 @@ NMSPMM_API nmspmm_status_t nmspmm_run(const float *A, const float *Bc, const uin
                            float *C, int64_t m, int64_t n, int64_t k, int N,
                            int M, int V, hipStream_t stream);
 
+/* Activation of the output epilogue of nmspmm_run_ex. */
+typedef enum {
+    NMSPMM_ACT_NONE = 0,
+    NMSPMM_ACT_RELU = 1,   /* max(0, y) */
+    NMSPMM_ACT_GELU = 2    /* y * Phi(y) = 0.5 * y * (1 + erf(y / sqrt(2))), fp32 erff */
+} nmspmm_act_t;
+
+/* nmspmm_run with an output epilogue:
+ *   C[i][j] = act(alpha * (A * B_pruned)[i][j] + bias[j])
+ * alpha = M/N gives Eq. 1's leading factor (Sec. II-A), which nmspmm_run
+ * leaves out; bias (n fp32 values, DEVICE pointer, may be NULL: no bias) and
+ * act are the epilogue of a linear layer such as the Llama layers of
+ * Sec. IV-A (not part of the paper's operator).  Arguments, layout,
+ * asynchrony and errors as nmspmm_run, plus NMSPMM_ERR_INVALID_ARG for an
+ * unknown act and NMSPMM_ERR_UNSUPPORTED for a bias not aligned to 4 bytes.
+ * The epilogue is applied once per output, in fp32, after the whole sum over
+ * k (when the kernel splits k, by a second pass over C).  With alpha = 1,
+ * bias = NULL and NMSPMM_ACT_NONE the result is bit-identical to
+ * nmspmm_run. */
+NMSPMM_API nmspmm_status_t nmspmm_run_ex(const float *A, const float *Bc, const uint8_t *idx,
+                              float *C, int64_t m, int64_t n, int64_t k, int N,
+                              int M, int V, float alpha, const float *bias,
+                              nmspmm_act_t act, hipStream_t stream);
+
+/* nmspmm_compress on the GPU, for pruning on the fly (same selection rule,
+ * same output bytes as the host call: for every window and column block the
+ * N row-vectors of largest fp64 squared L2 norm, ties to the smaller offset,
+ * offsets increasing).  DEVICE pointers, all on the current HIP device;
+ * asynchronous on `stream`, allocates nothing.  B_dense: k x n fp32
+ * row-major, read only.  Bc: w x n fp32 and idx: w x q uint8 (w = (k/M)*N,
+ * q = n/V), overwritten.  k == 0 or n == 0 returns NMSPMM_OK without a
+ * launch.  NaN inputs are outside the contract (the output is then
+ * unspecified, every access still in bounds).  Errors:
+ * NMSPMM_ERR_INVALID_ARG (bad shape, null pointer with non-empty data),
+ * NMSPMM_ERR_UNSUPPORTED (a float pointer not aligned to 4 bytes, sizes
+ * beyond int64), NMSPMM_ERR_HIP (the launch failed). */
+NMSPMM_API nmspmm_status_t nmspmm_compress_device(const float *B_dense, int64_t k, int64_t n,
+                                       int N, int M, int V, float *Bc, uint8_t *idx,
+                                       hipStream_t stream);
+
 /* Host check of the pattern rules (Sec. II-A): every (group, block) has N
  * offsets, each < M, strictly increasing.  HOST pointer, O(w*q).
  * Returns NMSPMM_OK or NMSPMM_ERR_INVALID_ARG. */

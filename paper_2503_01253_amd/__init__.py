@@ -6,8 +6,9 @@ The compute lives in libnmspmm.so (hand-written gfx950 HIP kernels behind a
 C ABI declared in include/nmspmm.h); this package is its ctypes binding.
 """
 from .binding import (  # noqa: F401
-    EXPORTS, NMSPMM_ERR_HIP, NMSPMM_ERR_INVALID_ARG, NMSPMM_ERR_UNSUPPORTED, NMSPMM_OK,
-    NmSpmmError, lib, nmspmm_bc_elems, nmspmm_compress, nmspmm_idx_bytes,
-    nmspmm_kernel_name, nmspmm_run, nmspmm_run_ptr, nmspmm_status_string,
+    ACTS, EXPORTS, NMSPMM_ACT_GELU, NMSPMM_ACT_NONE, NMSPMM_ACT_RELU, NMSPMM_ERR_HIP,
+    NMSPMM_ERR_INVALID_ARG, NMSPMM_ERR_UNSUPPORTED, NMSPMM_OK, NmSpmmError, lib,
+    nmspmm_bc_elems, nmspmm_compress, nmspmm_compress_device, nmspmm_idx_bytes,
+    nmspmm_kernel_name, nmspmm_run, nmspmm_run_ex, nmspmm_run_ptr, nmspmm_status_string,
     nmspmm_validate_idx,
 )

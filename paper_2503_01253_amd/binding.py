@@ -19,9 +19,15 @@ NMSPMM_ERR_INVALID_ARG = 1
 NMSPMM_ERR_UNSUPPORTED = 2
 NMSPMM_ERR_HIP = 3
 
+NMSPMM_ACT_NONE = 0
+NMSPMM_ACT_RELU = 1
+NMSPMM_ACT_GELU = 2
+ACTS = {"none": NMSPMM_ACT_NONE, "relu": NMSPMM_ACT_RELU, "gelu": NMSPMM_ACT_GELU}
+
 EXPORTS = (
-    "nmspmm_bc_elems", "nmspmm_idx_bytes", "nmspmm_compress", "nmspmm_run",
-    "nmspmm_validate_idx", "nmspmm_status_string", "nmspmm_kernel_name",
+    "nmspmm_bc_elems", "nmspmm_idx_bytes", "nmspmm_compress", "nmspmm_compress_device",
+    "nmspmm_run", "nmspmm_run_ex", "nmspmm_validate_idx", "nmspmm_status_string",
+    "nmspmm_kernel_name",
 )
 
 
@@ -60,6 +66,10 @@ def lib():
     L.nmspmm_status_string.restype = ctypes.c_char_p
     L.nmspmm_kernel_name.argtypes = [I64, I64, I64, I, I, I]
     L.nmspmm_kernel_name.restype = ctypes.c_char_p
+    L.nmspmm_run_ex.argtypes = [P, P, P, P, I64, I64, I64, I, I, I, ctypes.c_float, P, I, P]
+    L.nmspmm_run_ex.restype = I
+    L.nmspmm_compress_device.argtypes = [P, I64, I64, I, I, I, P, P, P]
+    L.nmspmm_compress_device.restype = I
     _lib = L
     return L
 
@@ -117,28 +127,72 @@ def nmspmm_run_ptr(A: int, Bc: int, idx: int, C: int, m: int, n: int, k: int,
     return int(lib().nmspmm_run(A, Bc, idx, C, m, n, k, N, M, V, stream))
 
 
+def _check_tensors(torch, C, specs):
+    for name, t, dt, numel in specs:
+        if not isinstance(t, torch.Tensor) or t.dtype != dt or not t.is_cuda or not t.is_contiguous():
+            raise TypeError(f"{name} must be a contiguous CUDA tensor of {dt}")
+        if t.device != C.device:
+            raise ValueError(f"{name} is on {t.device}, {C.device} expected")
+        if t.numel() != numel:
+            raise ValueError(f"{name} has {t.numel()} elements, expected {numel}")
+
+
 def nmspmm_run(A, Bc, idx, C, m: int, n: int, k: int, N: int, M: int, V: int, stream=None):
     """C = A * B_pruned on the GPU, asynchronously on ``stream`` (a
     torch.cuda.Stream; default: torch's current stream).  A (m x k), Bc
     (w x n), C (m x n) are contiguous fp32 CUDA tensors, idx (w x q) a
     contiguous uint8 CUDA tensor, all on one device."""
+    return nmspmm_run_ex(A, Bc, idx, C, m, n, k, N, M, V, stream=stream, _name="nmspmm_run")
+
+
+def nmspmm_run_ex(A, Bc, idx, C, m: int, n: int, k: int, N: int, M: int, V: int,
+                  alpha: float = 1.0, bias=None, act: str = "none", stream=None,
+                  _name: str = "nmspmm_run_ex"):
+    """C = act(alpha * (A * B_pruned) + bias) on the GPU (alpha = M/N is Eq. 1's
+    factor; bias an n-element fp32 CUDA tensor or None; act "none", "relu" or
+    "gelu").  Tensors and stream as for nmspmm_run."""
     import torch
     L = lib()
-    for name, t, dt in (("A", A, torch.float32), ("Bc", Bc, torch.float32),
-                        ("idx", idx, torch.uint8), ("C", C, torch.float32)):
-        if not isinstance(t, torch.Tensor) or t.dtype != dt or not t.is_cuda or not t.is_contiguous():
-            raise TypeError(f"{name} must be a contiguous CUDA tensor of {dt}")
-        if t.device != C.device:
-            raise ValueError(f"{name} is on {t.device}, C on {C.device}")
     w = (k // M) * N if M > 0 else 0
     q = n // V if V > 0 else 0
-    for name, t, numel in (("A", A, m * k), ("Bc", Bc, w * n), ("idx", idx, w * q), ("C", C, m * n)):
-        if t.numel() != numel:
-            raise ValueError(f"{name} has {t.numel()} elements, expected {numel}")
+    specs = [("A", A, torch.float32, m * k), ("Bc", Bc, torch.float32, w * n),
+             ("idx", idx, torch.uint8, w * q), ("C", C, torch.float32, m * n)]
+    if bias is not None:
+        specs.append(("bias", bias, torch.float32, n))
+    _check_tensors(torch, C, specs)
+    if act not in ACTS:
+        raise ValueError(f"act must be one of {sorted(ACTS)}")
     if stream is None:
         stream = torch.cuda.current_stream(C.device)
     with torch.cuda.device(C.device):
-        st = L.nmspmm_run(A.data_ptr(), Bc.data_ptr(), idx.data_ptr(), C.data_ptr(),
-                          m, n, k, N, M, V, stream.cuda_stream)
-    _check("nmspmm_run", st)
+        if _name == "nmspmm_run":
+            st = L.nmspmm_run(A.data_ptr(), Bc.data_ptr(), idx.data_ptr(), C.data_ptr(),
+                              m, n, k, N, M, V, stream.cuda_stream)
+        else:
+            st = L.nmspmm_run_ex(A.data_ptr(), Bc.data_ptr(), idx.data_ptr(), C.data_ptr(),
+                                 m, n, k, N, M, V, float(alpha),
+                                 None if bias is None else bias.data_ptr(), ACTS[act],
+                                 stream.cuda_stream)
+    _check(_name, st)
     return C
+
+
+def nmspmm_compress_device(B_dense, Bc, idx, N: int, M: int, V: int, stream=None):
+    """Device packer: B_dense (k x n fp32 CUDA tensor) -> Bc (w x n fp32) and
+    idx (w x q uint8), caller-allocated CUDA tensors, asynchronously on
+    ``stream`` (default: torch's current stream)."""
+    import torch
+    if B_dense.dim() != 2:
+        raise ValueError("B_dense must be 2-D")
+    k, n = B_dense.shape
+    w = (k // M) * N if M > 0 else 0
+    q = n // V if V > 0 else 0
+    _check_tensors(torch, B_dense, [("B_dense", B_dense, torch.float32, k * n),
+                                    ("Bc", Bc, torch.float32, w * n), ("idx", idx, torch.uint8, w * q)])
+    if stream is None:
+        stream = torch.cuda.current_stream(B_dense.device)
+    with torch.cuda.device(B_dense.device):
+        st = lib().nmspmm_compress_device(B_dense.data_ptr(), k, n, N, M, V, Bc.data_ptr(),
+                                          idx.data_ptr(), stream.cuda_stream)
+    _check("nmspmm_compress_device", st)
+    return Bc, idx

@@ -55,30 +55,30 @@ extern "C" nmspmm_status_t nmspmm_compress(const float *B_dense, int64_t k, int6
     const int64_t groups = k / M, blocks = n / V, pairs = groups * blocks;
     // (window, column block) pairs are independent; split them over threads.
     auto pack_range = [=](int64_t lo, int64_t hi) {
-    for (int64_t pair = lo; pair < hi; ++pair) {
-        const int64_t g = pair / blocks, b = pair % blocks;
-        const float *win = B_dense + g * M * n + b * V;
-        // Squared L2 norm of each length-V row-vector.  fp32 squares are exact
-        // in fp64 and the columns are added left to right, so the score (and
-        // therefore every tie) is reproducible bit for bit.
-        double norm2[256];
-        int order[256];
-        for (int o = 0; o < M; ++o) {
-            const float *v = win + (int64_t)o * n;
-            double s = 0.0;
-            for (int c = 0; c < V; ++c) s += (double)v[c] * (double)v[c];
-            norm2[o] = s;
-            order[o] = o;
+        for (int64_t pair = lo; pair < hi; ++pair) {
+            const int64_t g = pair / blocks, b = pair % blocks;
+            const float *win = B_dense + g * M * n + b * V;
+            // Squared L2 norm of each length-V row-vector.  fp32 squares are exact
+            // in fp64 and the columns are added left to right, so the score (and
+            // therefore every tie) is reproducible bit for bit.
+            double norm2[256];
+            int order[256];
+            for (int o = 0; o < M; ++o) {
+                const float *v = win + (int64_t)o * n;
+                double s = 0.0;
+                for (int c = 0; c < V; ++c) s += (double)v[c] * (double)v[c];
+                norm2[o] = s;
+                order[o] = o;
+            }
+            // Largest norms first, equal norms in offset order; keep the first N.
+            std::stable_sort(order, order + M, [&](int x, int y) { return norm2[x] > norm2[y]; });
+            std::sort(order, order + N);
+            for (int r = 0; r < N; ++r) {
+                const int64_t u = g * N + r;
+                idx[u * blocks + b] = (uint8_t)order[r];
+                std::memcpy(Bc + u * n + b * V, win + (int64_t)order[r] * n, sizeof(float) * (size_t)V);
+            }
         }
-        // Largest norms first, equal norms in offset order; keep the first N.
-        std::stable_sort(order, order + M, [&](int x, int y) { return norm2[x] > norm2[y]; });
-        std::sort(order, order + N);
-        for (int r = 0; r < N; ++r) {
-            const int64_t u = g * N + r;
-            idx[u * blocks + b] = (uint8_t)order[r];
-            std::memcpy(Bc + u * n + b * V, win + (int64_t)order[r] * n, sizeof(float) * (size_t)V);
-        }
-    }
     };
     const int64_t work = pairs * (int64_t)M * V;
     const int64_t nthreads = std::max<int64_t>(

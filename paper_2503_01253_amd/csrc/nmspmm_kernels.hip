@@ -34,7 +34,7 @@ constexpr int GEN_ROWS = 8;
 
 __global__ __launch_bounds__(GEN_COLS) void nm_general_kernel(
     const float *__restrict__ A, const float *__restrict__ Bc, const uint8_t *__restrict__ idx,
-    float *__restrict__ C, int64_t m, int64_t n, int64_t k, int N, int M, int V)
+    float *__restrict__ C, int64_t m, int64_t n, int64_t k, int N, int M, int V, Epilogue epi)
 {
     const int64_t j = (int64_t)blockIdx.x * GEN_COLS + threadIdx.x;
     if (j >= n) return;
@@ -53,8 +53,18 @@ __global__ __launch_bounds__(GEN_COLS) void nm_general_kernel(
         }
 #pragma unroll
         for (int r = 0; r < GEN_ROWS; ++r)
-            if (i0 + r < m) C[(i0 + r) * n + j] = acc[r];
+            if (i0 + r < m) C[(i0 + r) * n + j] = apply_epilogue(epi, acc[r], j);
     }
+}
+
+// The epilogue of a split-k launch, once the atomic sums are complete: one
+// pass over C.
+__global__ __launch_bounds__(256) void nm_epilogue_kernel(float *__restrict__ C, int64_t count,
+                                                           int64_t n, Epilogue epi)
+{
+    const int64_t stride = (int64_t)gridDim.x * 256;
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < count; i += stride)
+        C[i] = apply_epilogue(epi, C[i], i % n);
 }
 
 // Zero C before a split-k launch accumulates into it (a kernel, not a
@@ -335,20 +345,25 @@ Plan make_plan(const float *A, const float *Bc, const float *C, int64_t m, int64
 }
 
 hipError_t launch_general(const float *A, const float *Bc, const uint8_t *idx, float *C,
-                          int64_t m, int64_t n, int64_t k, int N, int M, int V, hipStream_t stream)
+                          int64_t m, int64_t n, int64_t k, int N, int M, int V, const Epilogue &epi,
+                          hipStream_t stream)
 {
     const int64_t gx = (n + GEN_COLS - 1) / GEN_COLS;
     const int64_t gy = std::min<int64_t>((m + GEN_ROWS - 1) / GEN_ROWS, 65535);
     if (gx > INT32_MAX) return hipErrorInvalidValue;
     hipLaunchKernelGGL(nm_general_kernel, dim3((unsigned)gx, (unsigned)gy), dim3(GEN_COLS), 0,
-                       stream, A, Bc, idx, C, m, n, k, N, M, V);
+                       stream, A, Bc, idx, C, m, n, k, N, M, V, epi);
     return hipGetLastError();
 }
 
-hipError_t launch_plan(const Plan &p, const float *A, const float *Bc, const uint8_t *idx, float *C,
-                       int64_t m, int64_t n, int64_t k, int N, int M, int V, hipStream_t stream)
+bool trivial(const Epilogue &e) { return e.alpha == 1.f && !e.bias && e.act == NMSPMM_ACT_NONE; }
+
+hipError_t launch_main(const Plan &p, const float *A, const float *Bc, const uint8_t *idx, float *C,
+                       int64_t m, int64_t n, int64_t k, int N, int M, int V, const Epilogue &epi,
+                       hipStream_t stream)
 {
-    if (p.kind == Kind::General) return launch_general(A, Bc, idx, C, m, n, k, N, M, V, stream);
+    if (p.kind == Kind::General)
+        return launch_general(A, Bc, idx, C, m, n, k, N, M, V, epi, stream);
     if (p.splits > 1) {
         const int64_t count = m * n;
         const int64_t blocks = std::min<int64_t>((count + 255) / 256, 4096);
@@ -372,6 +387,7 @@ hipError_t launch_plan(const Plan &p, const float *A, const float *Bc, const uin
         s.tiles_m = p.tiles_m;
         s.tiles_n = p.tiles_n;
         s.cw = p.CW;
+        s.epi = epi;
         return launch_skinny(p.BV, p.QPW, p.COLS, s, stream);
     }
     TiledArgs a;
@@ -390,7 +406,23 @@ hipError_t launch_plan(const Plan &p, const float *A, const float *Bc, const uin
     a.splits = p.splits;
     a.tiles_m = p.tiles_m;
     a.tiles_n = p.tiles_n;
+    a.epi = epi;
     return p.tile->launch(p.BV, p.KA, p.NQ, a, stream);
+}
+
+// The kernel(s) of a plan, then, when k was split across workgroups and the
+// epilogue does something, one pass over C that applies it.
+hipError_t launch_plan(const Plan &p, const float *A, const float *Bc, const uint8_t *idx, float *C,
+                       int64_t m, int64_t n, int64_t k, int N, int M, int V, const Epilogue &epi,
+                       hipStream_t stream)
+{
+    hipError_t e = launch_main(p, A, Bc, idx, C, m, n, k, N, M, V, epi, stream);
+    if (e != hipSuccess || p.kind == Kind::General || p.splits == 1 || trivial(epi)) return e;
+    const int64_t count = m * n;
+    const int64_t blocks = std::min<int64_t>((count + 255) / 256, 4096);
+    hipLaunchKernelGGL(nm_epilogue_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, C, count, n,
+                       epi);
+    return hipGetLastError();
 }
 
 }  // namespace
@@ -420,19 +452,33 @@ extern "C" const char *nmspmm_kernel_name(int64_t m, int64_t n, int64_t k, int N
     return buf;
 }
 
-extern "C" nmspmm_status_t nmspmm_run(const float *A, const float *Bc, const uint8_t *idx,
-                                      float *C, int64_t m, int64_t n, int64_t k, int N, int M,
-                                      int V, hipStream_t stream)
+extern "C" nmspmm_status_t nmspmm_run_ex(const float *A, const float *Bc, const uint8_t *idx,
+                                         float *C, int64_t m, int64_t n, int64_t k, int N, int M,
+                                         int V, float alpha, const float *bias, nmspmm_act_t act,
+                                         hipStream_t stream)
 {
     if (!shape_ok(m, n, k, N, M, V)) return NMSPMM_ERR_INVALID_ARG;
+    if (act != NMSPMM_ACT_NONE && act != NMSPMM_ACT_RELU && act != NMSPMM_ACT_GELU)
+        return NMSPMM_ERR_INVALID_ARG;
     if (!sizes_fit(m, n, k)) return NMSPMM_ERR_UNSUPPORTED;
     if (m == 0 || n == 0) return NMSPMM_OK;
     if (!C) return NMSPMM_ERR_INVALID_ARG;
     if (k > 0 && (!A || !Bc || !idx)) return NMSPMM_ERR_INVALID_ARG;
-    if (!aligned(C, 4) || (k > 0 && (!aligned(A, 4) || !aligned(Bc, 4))))
+    if (!aligned(C, 4) || (k > 0 && (!aligned(A, 4) || !aligned(Bc, 4))) || !aligned(bias, 4))
         return NMSPMM_ERR_UNSUPPORTED;
     const Plan p = make_plan(A, Bc, C, m, n, k, N, M, V);
     if (p.kind == Kind::None) return NMSPMM_OK;
-    const hipError_t e = launch_plan(p, A, Bc, idx, C, m, n, k, N, M, V, stream);
+    Epilogue epi;
+    epi.alpha = alpha;
+    epi.bias = bias;
+    epi.act = act;
+    const hipError_t e = launch_plan(p, A, Bc, idx, C, m, n, k, N, M, V, epi, stream);
     return e == hipSuccess ? NMSPMM_OK : NMSPMM_ERR_HIP;
+}
+
+extern "C" nmspmm_status_t nmspmm_run(const float *A, const float *Bc, const uint8_t *idx,
+                                      float *C, int64_t m, int64_t n, int64_t k, int N, int M,
+                                      int V, hipStream_t stream)
+{
+    return nmspmm_run_ex(A, Bc, idx, C, m, n, k, N, M, V, 1.f, nullptr, NMSPMM_ACT_NONE, stream);
 }

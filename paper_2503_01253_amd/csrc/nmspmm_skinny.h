@@ -6,6 +6,8 @@
 
 #include <cstdint>
 
+#include "nmspmm_tiled.h"
+
 namespace nmspmm {
 
 struct SkinnyArgs {
@@ -18,6 +20,7 @@ struct SkinnyArgs {
     int splits;          // workgroups per output tile along k (>1: atomic adds into a zeroed C)
     int tiles_m, tiles_n;
     int cw;              // windows per staged chunk of A: cw * M <= skinny_chunk_cols()
+    Epilogue epi;        // applied by the stores when splits == 1
 };
 
 int skinny_rows();        // rows of C per workgroup

@@ -244,7 +244,7 @@ __global__ __launch_bounds__(SK_NT) void nm_skinny_kernel(SkinnyArgs p)
         const int64_t row = row0 + e / COLS, col = col0 + e % COLS;
         if (row >= m || col >= n) continue;
         if (p.splits == 1)
-            p.C[row * n + col] = sum;
+            p.C[row * n + col] = apply_epilogue(p.epi, sum, col);
         else
             unsafeAtomicAdd(p.C + row * n + col, sum);
     }

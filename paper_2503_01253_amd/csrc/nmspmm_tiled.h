@@ -108,6 +108,25 @@ struct Shape {
                                  (B_FLOATS * 4) % T::NT == 0 && B_LANE % 4 == 0 && B_CNT >= 1;
 };
 
+// Output epilogue act(alpha * c + bias[j]) (see nmspmm_run_ex).
+struct Epilogue {
+    float alpha;
+    const float *bias;   // n values or null
+    int act;             // nmspmm_act_t
+};
+
+__device__ __forceinline__ float apply_epilogue(const Epilogue &e, float v, int64_t col)
+{
+    v *= e.alpha;
+    if (e.bias) v += e.bias[col];
+    if (e.act == 1) {
+        v = fmaxf(v, 0.f);
+    } else if (e.act == 2) {
+        v = 0.5f * v * (1.f + erff(v * 0.70710678118654752f));
+    }
+    return v;
+}
+
 struct TiledArgs {
     const float *A;
     const float *Bc;
@@ -119,6 +138,7 @@ struct TiledArgs {
     int stages;      // ceil((k/M) / (KA/M))
     int splits;      // split-k factor (>1: atomic accumulation into a zeroed C)
     int tiles_m, tiles_n;
+    Epilogue epi;    // applied by the stores when splits == 1
 };
 
 // Workgroups are dispatched round-robin over the 8 XCDs.  Renumber them so
@@ -418,10 +438,11 @@ __global__ __launch_bounds__(T::NT) void nm_tiled_kernel(TiledArgs p)
                     if (p.splits == 1) {
                         bvec out;
                         if constexpr (BV == 1) {
-                            out = acc[cg][rc][t][0][e];
+                            out = apply_epilogue(p.epi, acc[cg][rc][t][0][e], col);
                         } else {
 #pragma unroll
-                            for (int s = 0; s < BV; ++s) out[s] = acc[cg][rc][t][s][e];
+                            for (int s = 0; s < BV; ++s)
+                                out[s] = apply_epilogue(p.epi, acc[cg][rc][t][s][e], col + s);
                         }
                         *reinterpret_cast<bvec *>(dst) = out;
                     } else {

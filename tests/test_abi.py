@@ -22,7 +22,7 @@ def declared_symbols():
 
 def test_library_exports_every_declared_symbol():
     names = declared_symbols()
-    assert len(names) == 7
+    assert len(names) == 9
     assert sorted(nm.EXPORTS) == names
     L = nm.lib()
     for name in names:
@@ -125,3 +125,19 @@ def test_kernel_selection():
     assert nm.nmspmm_kernel_name(5, 12, 8, 1, 4, 1) == "nm_general_kernel"
     assert nm.nmspmm_kernel_name(0, 64, 64, 4, 32, 32) == "none"
     assert nm.nmspmm_kernel_name(8, 64, 65, 4, 32, 32) == "invalid"
+
+
+def test_run_ex_and_compress_device_argument_checks():
+    L = nm.lib()
+    # unknown activation, before anything else is looked at
+    assert L.nmspmm_run_ex(0, 0, 0, 0, 8, 64, 64, 4, 32, 32, 1.0, None, 7, None) == nm.NMSPMM_ERR_INVALID_ARG
+    # empty problem: OK without a launch; misaligned bias: rejected before a launch
+    assert L.nmspmm_run_ex(0, 0, 0, 0, 0, 64, 64, 4, 32, 32, 2.0, None, 1, None) == nm.NMSPMM_OK
+    assert L.nmspmm_run_ex(4096, 4096, 4096, 4096, 8, 64, 64, 4, 32, 32, 1.0, 4098, 0, None) == \
+        nm.NMSPMM_ERR_UNSUPPORTED
+    assert L.nmspmm_run_ex(0, 0, 0, 0, 8, 64, 64, 4, 32, 32, 1.0, None, 0, None) == nm.NMSPMM_ERR_INVALID_ARG
+    # device packer: shape rules, empty sizes, null and misaligned pointers
+    assert L.nmspmm_compress_device(0, 64, 60, 4, 32, 32, 0, 0, None) == nm.NMSPMM_ERR_INVALID_ARG
+    assert L.nmspmm_compress_device(0, 0, 64, 4, 32, 32, 0, 0, None) == nm.NMSPMM_OK
+    assert L.nmspmm_compress_device(0, 64, 64, 4, 32, 32, 0, 0, None) == nm.NMSPMM_ERR_INVALID_ARG
+    assert L.nmspmm_compress_device(4098, 64, 64, 4, 32, 32, 4096, 4096, None) == nm.NMSPMM_ERR_UNSUPPORTED

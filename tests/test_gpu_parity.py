@@ -286,3 +286,118 @@ def test_dense_comparator_is_true_fp32():
     C = torch.matmul(to_dev(A), to_dev(Bp)).cpu().numpy()
     r = oracle.check(C, oracle.spmm(A, Bc, idx, m, n, k, N, M, V), oracle.bound(A, Bc, idx, m, n, k, N, M, V))
     assert r, r
+
+
+# ---- output epilogue (nmspmm_run_ex) ----
+# one shape per kernel family: tiled (one workgroup per tile), tiled split-k,
+# streaming, streaming split-k, general kernel
+EPI_SHAPES = [
+    (2048, 128, 8192, 8, 32, 32),
+    (300, 256, 1088, 8, 32, 32),
+    (16, 2048, 640, 4, 32, 128),
+    (16, 512, 4096, 4, 32, 64),
+    (17, 24, 10, 3, 8, 2),
+]
+
+
+def run_ex(A, Bc, idx, m, n, k, N, M, V, alpha, bias, act):
+    dC = torch.full((m, n), float("nan"), dtype=torch.float32, device="cuda")
+    nm.nmspmm_run_ex(to_dev(A), to_dev(Bc), to_dev(idx), dC, m, n, k, N, M, V, alpha=alpha,
+                     bias=None if bias is None else to_dev(bias), act=act)
+    torch.cuda.synchronize()
+    return dC.cpu().numpy()
+
+
+@pytest.mark.parametrize("act", ["none", "relu", "gelu"])
+@pytest.mark.parametrize("shape", EPI_SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_run_ex_epilogue(shape, act):
+    """act(alpha * C + bias) against the oracle's epilogue on its fp64 product;
+    alpha = M/N (Eq. 1's factor).  Bound: the product's bar propagated through
+    alpha and the activation (|d act| <= 1.13 |d y|), plus fp32 rounding of the
+    epilogue itself."""
+    m, k, n, N, M, V = shape
+    say(f"[epilogue] {shape} {act} kernel={nm.nmspmm_kernel_name(m, n, k, N, M, V)}")
+    A, Bp, _ = make_inputs(m, k, n, N, M, V, 40 + m, "normal")
+    Bc, idx = oracle.compress(Bp, N, M, V)
+    bias = np.random.default_rng(m).standard_normal(n).astype(np.float32)
+    alpha = M / N
+    C_ref = oracle.spmm(A, Bc, idx, m, n, k, N, M, V)
+    Bnd = oracle.bound(A, Bc, idx, m, n, k, N, M, V)
+    Y_ref = oracle.epilogue(C_ref, alpha, bias, act)
+    y_ref = oracle.epilogue(C_ref, alpha, bias, "none")
+    Y = run_ex(A, Bc, idx, m, n, k, N, M, V, alpha, bias, act).astype(np.float64)
+    tol = (1.2 * (alpha * 1e-5 * Bnd + 2.0 ** -22 * (np.abs(alpha * C_ref) + np.abs(bias)))
+           + 4e-7 * (np.abs(y_ref) + np.abs(Y_ref)) + 1e-30)
+    err = np.abs(Y - Y_ref)
+    assert np.isfinite(Y).all()
+    assert bool((err <= tol).all()), f"worst err/tol {float((err / tol).max()):.3g}"
+
+
+@pytest.mark.parametrize("shape", EPI_SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_run_ex_exact_on_integers(shape):
+    """Small integers, a power-of-two alpha and an integer bias: every value is
+    exact in fp32, so the epilogue must match the oracle bit for bit."""
+    m, k, n, N, M, V = shape
+    A, Bp, _ = make_inputs(m, k, n, N, M, V, 3 + m, "int")
+    Bc, idx = oracle.compress(Bp, N, M, V)
+    bias = np.random.default_rng(n).integers(-50, 50, n).astype(np.float32)
+    C_ref = oracle.spmm(A, Bc, idx, m, n, k, N, M, V)
+    for alpha, act in ((4.0, "relu"), (0.5, "none")):
+        Y = run_ex(A, Bc, idx, m, n, k, N, M, V, alpha, bias, act)
+        assert bool(np.array_equal(Y.astype(np.float64), oracle.epilogue(C_ref, alpha, bias, act)))
+
+
+def test_run_ex_trivial_epilogue_is_nmspmm_run():
+    m, k, n, N, M, V = 2048, 128, 8192, 8, 32, 32
+    A, Bp, _ = make_inputs(m, k, n, N, M, V, 12)
+    Bc, idx = nm.nmspmm_compress(Bp, N, M, V)
+    C = gpu_run(A, Bc, idx, m, n, k, N, M, V)
+    Y = run_ex(A, Bc, idx, m, n, k, N, M, V, 1.0, None, "none")
+    assert bool(np.array_equal(C.view(np.uint32), Y.view(np.uint32)))
+
+
+# ---- device packer (nmspmm_compress_device) ----
+PACK_SHAPES = [
+    (64, 96, 4, 32, 32), (256, 256, 16, 32, 32), (128, 128, 8, 32, 64), (48, 30, 3, 8, 3),
+    (28, 21, 2, 7, 3), (64, 64, 32, 32, 32), (64, 64, 1, 32, 16), (512, 256, 12, 32, 32),
+    (512, 48, 5, 256, 16), (1024, 4096, 4, 32, 64),
+]
+
+
+def device_pack(B, N, M, V):
+    k, n = B.shape
+    w = (k // M) * N
+    dBc = torch.full((w, n), float("nan"), dtype=torch.float32, device="cuda")
+    didx = torch.full((w, n // V), 255, dtype=torch.uint8, device="cuda")
+    nm.nmspmm_compress_device(to_dev(B), dBc, didx, N, M, V)
+    torch.cuda.synchronize()
+    return dBc.cpu().numpy(), didx.cpu().numpy()
+
+
+@pytest.mark.parametrize("kind", ["pruned", "dense", "ties", "zeros"])
+@pytest.mark.parametrize("shape", PACK_SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_compress_device_matches_oracle_byte_for_byte(shape, kind):
+    k, n, N, M, V = shape
+    if kind == "pruned":
+        _, B, _ = make_inputs(1, k, n, N, M, V, seed=k + n, dist="normal")
+    elif kind == "dense":
+        B = np.random.default_rng(k * n).standard_normal((k, n)).astype(np.float32)
+    elif kind == "ties":   # repeated row-vectors: every selection is decided by the tie rule
+        B = np.repeat(np.random.default_rng(7).integers(-2, 3, (k // 2, n)), 2, axis=0).astype(np.float32)
+    else:
+        B = np.zeros((k, n), np.float32)
+    Bc, idx = device_pack(B, N, M, V)
+    Bc_o, idx_o = oracle.compress(B, N, M, V)
+    assert np.array_equal(idx, idx_o)
+    assert Bc.tobytes() == Bc_o.tobytes()
+
+
+def test_device_pack_then_run_matches_host_pipeline():
+    m, k, n, N, M, V = 512, 2048, 1024, 8, 32, 32
+    A, Bp, _ = make_inputs(m, k, n, N, M, V, 77)
+    Bc, idx = device_pack(Bp, N, M, V)
+    Bc_h, idx_h = nm.nmspmm_compress(Bp, N, M, V)
+    assert np.array_equal(idx, idx_h) and Bc.tobytes() == Bc_h.tobytes()
+    C = gpu_run(A, Bc, idx, m, n, k, N, M, V)
+    r = oracle.check(C, oracle.spmm(A, Bc_h, idx_h, m, n, k, N, M, V), oracle.bound(A, Bc_h, idx_h, m, n, k, N, M, V))
+    assert r, r
