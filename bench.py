@@ -43,8 +43,8 @@ CACHE_BYTES = 288 << 20      # 256 MB Infinity Cache + 8 x 4 MB L2
 # reads for a copy kernel of known size.  Keyed by workload, kernel variant
 # and the hash of that variant's device sources: null once any differs.
 TRAFFIC = {
-    ("R2", "nm_tiled_kernel<256x256,bv2,ka32,nq4>,split1", "414b64ea4482fd16"): {
-        "fetch_kib": 132238.8, "fetch_factor": 1.99995,
+    ("R2", "nm_tiled_kernel<256x256,bv2,ka32,nq4>,split1", "44e45721f424f383"): {
+        "fetch_kib": 132651.2, "fetch_factor": 1.99995,
         "write_kib": 65536.0, "write_factor": 1.0,
     },
 }
@@ -265,6 +265,49 @@ def measure(torch, nm, run, steps, warmup, with_dense, graph=False, warm_seconds
     return res, w
 
 
+def measure_extras(torch, nm):
+    """The steps beside the product: the fused epilogue of nmspmm_run_ex on the
+    MLP-shaped run (alpha = M/N, bias, GELU, against the plain product), and
+    the device packer nmspmm_compress_device on the headline's dense B."""
+    out = {}
+    r = RUNS["R4"]
+    w = Workload(r, torch, nm, min_copies=2)
+    bias = torch.randn(r.n, device="cuda")
+    h = torch.cuda.current_stream().cuda_stream
+    L = nm.lib()
+
+    def ex(i):
+        a, b, x, c = w.ptrs[i % w.copies]
+        st = L.nmspmm_run_ex(a, b, x, c, r.m, r.n, r.k, r.N, r.M, r.V, float(r.M / r.N),
+                             bias.data_ptr(), nm.NMSPMM_ACT_GELU, h)
+        if st != 0:
+            raise RuntimeError(nm.nmspmm_status_string(st))
+    _, plain = time_launches(torch, lambda i: w.launch(i, h), 20, 3, 0.2)
+    _, fused = time_launches(torch, ex, 20, 3, 0.2)
+    out["epilogue"] = {
+        "workload": r.describe(), "epilogue": "gelu(M/N * C + bias)",
+        "kernel": nm.nmspmm_kernel_name(r.m, r.n, r.k, r.N, r.M, r.V),
+        "plain_ms": statistics.median(plain), "fused_ms": statistics.median(fused),
+    }
+    w.free()
+    del bias
+    r = RUNS["R2"]
+    A, Bp, _ = make_run(r)
+    dB = torch.from_numpy(Bp).cuda()
+    wr = (r.k // r.M) * r.N
+    dBc = torch.empty((wr, r.n), dtype=torch.float32, device="cuda")
+    didx = torch.empty((wr, r.n // r.V), dtype=torch.uint8, device="cuda")
+    _, per = time_launches(torch, lambda i: nm.nmspmm_compress_device(dB, dBc, didx, r.N, r.M, r.V),
+                           20, 3, 0.2)
+    ms = statistics.median(per)
+    moved = 4.0 * r.k * r.n + 4.0 * wr * r.n + wr * (r.n // r.V)
+    out["device_compress"] = {"workload": f"B of {r.name}: {r.k} x {r.n}, {r.N}:{r.M}, V={r.V}",
+                              "ms": ms, "gb_s": moved / (ms * 1e-3) / 1e9}
+    del dB, dBc, didx
+    torch.cuda.empty_cache()
+    return out
+
+
 def device_clocks():
     """Current clocks as rocm-smi reports them (None where it is unavailable)."""
     import subprocess
@@ -388,6 +431,12 @@ def main():
             table.append(row)
             torch.cuda.empty_cache()
 
+    extras = {}
+    if not args.no_sweep:
+        log("[bench] epilogue and device packer")
+        extras = measure_extras(torch, nm)
+        log(f"[bench] extras {json.dumps(extras)}")
+
     ms = head["ms_per_step"]
     line = {
         "metric": "effective TFLOPS (2*m*n*k*N/M)",
@@ -412,6 +461,7 @@ def main():
                           "pct_of_fp32_peak_50_62.5_75_87.5": [96, 93, 95, 88]},
         "sweep": sweep,
         "shape_sparsity_table": table,
+        **extras,
         "device": torch.cuda.get_device_name(0),
         "device_clocks": device_clocks(),
     }
