@@ -269,10 +269,11 @@ Plan make_plan(const float *A, const float *Bc, const float *C, int64_t m, int64
     if ((int64_t)32 * n * 4 >= (int64_t(1) << 31)) return p;
 
     // Stage depth: the smallest KA (a multiple of 32 and of M) whose stage
-    // holds at least 16 compressed rows for the large tiles (8 for the tiles
-    // with few accumulators per lane, which share a CU between workgroups
-    // and prefer a small LDS ring), so every stage carries enough MFMA work
-    // to cover its fixed cost; deeper ones are tried if it does not fit.
+    // holds at least 16 compressed rows (8 for the tiles with few
+    // accumulators per lane on grids of more tiles than CUs: they share a CU
+    // between two workgroups and want a small LDS ring), so every stage
+    // carries enough MFMA work to cover its fixed cost; deeper ones are tried
+    // if it does not fit.
     auto ka_list = [&](int min_rows, int *order) {
         int cnt = 0;
         for (int KA : {32, 64, 128})
@@ -302,7 +303,10 @@ Plan make_plan(const float *A, const float *Bc, const float *C, int64_t m, int64
         if (!cand[j]) continue;
         const int bv = bv_for(cand[j]->MI, V);
         if (bv == 0 || !aligned(C, 4 * bv)) continue;
-        const bool small = acc_per_lane(*cand[j]) <= 64;
+        // the shallow rule pays off only when the grid has more tiles than
+        // CUs, so that a second workgroup per CU has work to bring
+        const int64_t tiles_c = ((m + cand[j]->BM - 1) / cand[j]->BM) * ((n + cand[j]->BN - 1) / cand[j]->BN);
+        const bool small = acc_per_lane(*cand[j]) <= 64 && tiles_c > 256;
         const int *order = small ? ka_small : ka_order;
         for (int i = 0; i < (small ? nks : nka) && !tile; ++i) {
             const int nq = stage_nq(order[i], (order[i] / M) * N);
