@@ -69,7 +69,10 @@ __global__ __launch_bounds__(SK_NT) void nm_skinny_kernel(SkinnyArgs p)
     // two A chunk buffers during the main loop; the reduction area after it
     __shared__ __align__(16) float lds[LDS_FLOATS];
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    // uniform across the wave; saying so keeps every address derived from
+    // it (the buffer resources included) in scalar registers
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int r = lane & 15, kq = lane >> 4;
     const int tiles_n = p.tiles_n;
     const int tile = blockIdx.x % (p.tiles_m * tiles_n);
@@ -83,14 +86,14 @@ __global__ __launch_bounds__(SK_NT) void nm_skinny_kernel(SkinnyArgs p)
     // windows [gb, ge) of this workgroup, walked in chunks of cw windows
     const int64_t G = k / M;
     const int64_t gps = (G + p.splits - 1) / p.splits;
-    const int64_t gb = min<int64_t>(G, (int64_t)split * gps), ge = min<int64_t>(G, gb + gps);
+    const int64_t gb = min64(G, (int64_t)split * gps), ge = min64(G, gb + gps);
     const int cw = p.cw;
     const int64_t nchunks = (ge - gb + cw - 1) / cw;
     // x / N for 0 <= x < 4096 as (x * invN) >> 20 (exact for N <= 256): a
     // chunk holds at most SK_KC / M * N <= 1024 compressed rows
     const uint32_t invN = ((1u << 20) + N - 1) / N;
 
-    const int rows_valid = (int)min<int64_t>(SK_ROWS, m - row0);
+    const int rows_valid = (int)min64(SK_ROWS, m - row0);
     const __amdgpu_buffer_rsrc_t a_rsrc =
         make_rsrc(p.A + row0 * k, (uint32_t)((int64_t)rows_valid * k * 4));
 
@@ -100,7 +103,7 @@ __global__ __launch_bounds__(SK_NT) void nm_skinny_kernel(SkinnyArgs p)
     auto dma_a = [&](int64_t c, int buf, bool valid) {
         const int64_t g0 = gb + c * cw;
         const int64_t kc0 = g0 * M;
-        const int64_t kcn = valid ? (min<int64_t>(ge, g0 + cw) - g0) * M : 0;
+        const int64_t kcn = valid ? (min64(ge, g0 + cw) - g0) * M : 0;
 #pragma unroll
         for (int i = 0; i < SK_DMA; ++i) {
             const int piece = wave * SK_DMA + i;
@@ -125,7 +128,7 @@ __global__ __launch_bounds__(SK_NT) void nm_skinny_kernel(SkinnyArgs p)
     auto chunk_rows = [&](int64_t c, int64_t &u0, int64_t &u1) {
         const int64_t w0 = gb + c * cw;
         u0 = w0 * N;
-        u1 = min<int64_t>(ge, w0 + cw) * N;
+        u1 = min64(ge, w0 + cw) * N;
     };
 
     // ---- one round's Bc operands and offsets, straight into registers ----
@@ -135,10 +138,10 @@ __global__ __launch_bounds__(SK_NT) void nm_skinny_kernel(SkinnyArgs p)
         const int64_t ub = u0 + ((int64_t)rd * SK_NW + wave) * QPW * 4;
 #pragma unroll
         for (int j = 0; j < QPW; ++j) {
-            const int64_t rows_left = max<int64_t>(0, u1 - (ub + 4 * j));
+            const int64_t rows_left = max64(0, u1 - (ub + 4 * j));
             const __amdgpu_buffer_rsrc_t b_rsrc =
                 make_rsrc(p.Bc + (ub + 4 * j) * n,
-                          (uint32_t)(min<int64_t>(rows_left, 4) * n * 4));
+                          (uint32_t)(min64(rows_left, 4) * n * 4));
             const int64_t u = ub + 4 * j + kq;
             const bool urow = u < u1;
 #pragma unroll

@@ -174,6 +174,12 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void *base, ui
 
 constexpr uint32_t OOB = 0x80000000u;  // an offset past every buffer used here
 
+// 64-bit integer min / max.  (HIP's device min / max templates resolve a call
+// whose two arguments differ in type, e.g. min<int64_t>(x, 4), to an overload
+// that computes in double.)
+__device__ __forceinline__ int64_t min64(int64_t a, int64_t b) { return a < b ? a : b; }
+__device__ __forceinline__ int64_t max64(int64_t a, int64_t b) { return a > b ? a : b; }
+
 // One buffer->LDS DMA instruction: lane l's W bytes from byte offset `off`
 // of the buffer land at dst + l*W.  (The width is spelled as a literal in
 // each branch: the builtin needs an integer constant that is not
@@ -240,7 +246,7 @@ __global__ __launch_bounds__(T::NT) void nm_tiled_kernel(TiledArgs p)
     // In a 32 x 32 chunk, lane l owns rows 4*(l%8)+t (t < 4) and columns
     // 4*(l/8)..+3: each load instruction covers 8 rows x 128 bytes.
     const int r8 = lane & 7, c8 = lane >> 3;
-    const int rows_valid = (int)min<int64_t>(BM, m - row0);
+    const int rows_valid = (int)min64(BM, m - row0);
     const __amdgpu_buffer_rsrc_t a_rsrc =
         make_rsrc(p.A + row0 * k, (uint32_t)((int64_t)rows_valid * k * 4));
     f32x4 ra[ACH][4];
@@ -295,7 +301,7 @@ __global__ __launch_bounds__(T::NT) void nm_tiled_kernel(TiledArgs p)
     auto dma_bx = [&](int s, int slot, bool valid) {
         unsigned char *bs = lds + slot * S::SLOT_BYTES + 4 * S::A_FLOATS;
         const int64_t u0 = (int64_t)s * RS;
-        const int64_t rows_left = valid ? max<int64_t>(0, min<int64_t>(RS, w - u0)) : 0;
+        const int64_t rows_left = valid ? max64(0, min64(RS, w - u0)) : 0;
         const __amdgpu_buffer_rsrc_t b_rsrc = make_rsrc(p.Bc + u0 * n, (uint32_t)(rows_left * n * 4));
 #pragma unroll
         for (int i = 0; i < S::B_CNT; ++i)

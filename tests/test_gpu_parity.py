@@ -361,6 +361,8 @@ PACK_SHAPES = [
     (64, 96, 4, 32, 32), (256, 256, 16, 32, 32), (128, 128, 8, 32, 64), (48, 30, 3, 8, 3),
     (28, 21, 2, 7, 3), (64, 64, 32, 32, 32), (64, 64, 1, 32, 16), (512, 256, 12, 32, 32),
     (512, 48, 5, 256, 16), (1024, 4096, 4, 32, 64),
+    # LDS tile cut to 6 of 32 blocks (ragged last tile); per-thread packer (1024-wide blocks)
+    (256, 512, 8, 128, 16), (64, 2048, 4, 32, 1024),
 ]
 
 
