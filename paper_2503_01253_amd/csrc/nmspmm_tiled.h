@@ -21,9 +21,10 @@
 //   X_s : the RST x (BN/V) offset bytes of D, one zero-extended dword each.
 // B_s and X_s are filled by buffer->LDS DMA.  All global reads go through
 // buffer descriptors whose range makes ragged m / n / k tails and padding
-// rows read zero.  The loads of stage s+1 are issued before stage s is
+// rows read zero.  The loads of stage s+1 are issued while stage s is
 // multiplied; the A registers are written to the other slot after it; one
-// barrier per stage.  Inside a stage the offsets of all MFMA K steps are read
+// barrier per stage.  (Deep stages of the tiles with few accumulators per
+// lane keep a single A_s slot, written after a second barrier.)  Inside a stage the offsets of all MFMA K steps are read
 // once (the index prefetch of Sec. III-C.2) and the operands of step j+1 are
 // read while step j is multiplied (the register double buffer of the same
 // section).
@@ -90,12 +91,26 @@ struct Shape {
     static constexpr int A_FLOATS = KA * T::AST;
     static constexpr int B_FLOATS = RST * T::BN;
     static constexpr int X_INTS = T::NT;
-    static constexpr int SLOT_BYTES = 4 * (A_FLOATS + B_FLOATS + X_INTS);
-    // LDS slots: two (the loads of stage s+1 are in flight while stage s is
-    // multiplied).  A three-slot ring with loads two stages ahead measured
-    // within 1-3 % on MI355X at the cost of a second set of A staging
-    // registers (and spills on the 128-accumulator tiles), so it is not used.
+    // LDS: two slots of B_s and X_s (the loads of stage s+1 are in flight
+    // while stage s is multiplied), and two slots of A_s where they fit.
+    // Otherwise, for the tiles with at most 64 accumulators per lane, one
+    // A_s slot: the A registers are the second buffer, and a barrier after
+    // the last read of A_s lets them overwrite it.  This is what lets those
+    // tiles take the deep stages of the sparsest levels: 128 x 256 at 4:32
+    // and KA = 128 measured 11 % faster than at KA = 64 on MI355X.  The
+    // 128-accumulator tiles have long enough stages at KA = 64; there the
+    // extra barrier and the doubled A load burst measured slower.  (A
+    // three-slot ring with loads two stages ahead measured within 1-3 % at
+    // the cost of a second set of A staging registers, and spills on the
+    // 128-accumulator tiles, so it is not used.)
     static constexpr int NSLOT = 2;
+    static constexpr int A_BYTES = 4 * A_FLOATS;
+    static constexpr int BX_BYTES = 4 * (B_FLOATS + X_INTS);
+    static constexpr bool TWO_A = NSLOT * (A_BYTES + BX_BYTES) <= LDS_CAPACITY;
+    static constexpr bool ONE_A_OK = T::BM * T::BN <= 64 * T::NT;
+    static constexpr int A_SLOTS = TWO_A ? 2 : 1;
+    static constexpr int SLOT_BYTES = A_BYTES + BX_BYTES;
+    static constexpr int LDS_BYTES = A_SLOTS * A_BYTES + NSLOT * BX_BYTES;
     // A: 32 x 32 chunks, one per wave at a time, each thread a 4 x 4 block
     static constexpr int A_CHUNKS = ((T::BM + 31) / 32) * (KA / 32);
     static constexpr int ACH = (A_CHUNKS + T::NW - 1) / T::NW;
@@ -103,7 +118,7 @@ struct Shape {
     static constexpr int B_LANE = B_FLOATS * 4 / T::NT;
     static constexpr int B_W = B_LANE % 16 == 0 ? 16 : 4;
     static constexpr int B_CNT = B_LANE / B_W;
-    static constexpr bool FITS = NSLOT * SLOT_BYTES <= LDS_CAPACITY && KA % 32 == 0 &&
+    static constexpr bool FITS = (TWO_A || ONE_A_OK) && LDS_BYTES <= LDS_CAPACITY && KA % 32 == 0 &&
                                  T::WN % CG == 0 && RST * QBMAX <= T::NT &&
                                  (B_FLOATS * 4) % T::NT == 0 && B_LANE % 4 == 0 && B_CNT >= 1;
 };
@@ -196,6 +211,16 @@ __device__ __forceinline__ void lds_dma(__amdgpu_buffer_rsrc_t rsrc, void *dst, 
         __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void *)dst, 1, (int)off, 0, 0, 0);
 }
 
+// Workgroup barrier after this wave's LDS accesses have completed; its
+// global loads and DMA stay in flight.
+__device__ __forceinline__ void lds_sync()
+{
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (0 << 8) | (3 << 14));  // lgkmcnt(0)
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
 // Workgroup barrier after this wave's outstanding global loads and DMA have
 // completed (vmcnt(0)) and its LDS accesses have too (lgkmcnt(0)).  No memory
 // fence beyond that is needed; the empty asm statements keep the compiler
@@ -218,10 +243,25 @@ __global__ __launch_bounds__(T::NT) void nm_tiled_kernel(TiledArgs p)
     typedef typename vec_of<BV>::type bvec;
     typedef typename vec_of<RPL>::type avec;
 
-    constexpr int NSLOT = S::NSLOT;
-    __shared__ __align__(16) unsigned char lds[NSLOT * S::SLOT_BYTES];
+    __shared__ __align__(16) unsigned char lds[S::LDS_BYTES];
+    // A_s of a slot, and B_s followed by X_s of a slot.  Two A slots: slot i
+    // is A_s, B_s, X_s at i * SLOT_BYTES, so that slot 0's B_s stays within
+    // the 16-bit offsets of LDS instructions.  One A slot: A_s, then the two
+    // B_s / X_s slots.
+    auto a_area = [&](int slot) -> unsigned char * {
+        if constexpr (S::TWO_A) return lds + slot * S::SLOT_BYTES;
+        else return lds;
+    };
+    auto bx_area = [&](int slot) -> unsigned char * {
+        if constexpr (S::TWO_A) return lds + slot * S::SLOT_BYTES + S::A_BYTES;
+        else return lds + S::A_BYTES + slot * S::BX_BYTES;
+    };
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    // uniform across the wave.  Saying so lets the 32x32 tiles keep their
+    // address math in scalar registers (measured 1-2 % faster); the 16x16
+    // tiles measured slightly slower with it.
+    const int wave = T::MI == 32 ? __builtin_amdgcn_readfirstlane(tid >> 6) : tid >> 6;
     int tm, tn, split;
     map_tile(blockIdx.x, gridDim.x, p.tiles_m, p.tiles_n, tm, tn, split);
     const int64_t row0 = (int64_t)tm * BM, col0 = (int64_t)tn * BN;
@@ -270,7 +310,7 @@ __global__ __launch_bounds__(T::NT) void nm_tiled_kernel(TiledArgs p)
         }
     };
     auto store_a = [&](int slot) {
-        float *As = reinterpret_cast<float *>(lds + slot * S::SLOT_BYTES);
+        float *As = reinterpret_cast<float *>(a_area(slot));
 #pragma unroll
         for (int ch = 0; ch < ACH; ++ch) {
             const int chunk = wave + ch * NW;
@@ -299,7 +339,7 @@ __global__ __launch_bounds__(T::NT) void nm_tiled_kernel(TiledArgs p)
     const bool x_ok = tid < RST * QB && x_ul < RS && b_first + x_bl < q;
     const uint32_t x_off = (uint32_t)(x_ul * q + b_first + x_bl);
     auto dma_bx = [&](int s, int slot, bool valid) {
-        unsigned char *bs = lds + slot * S::SLOT_BYTES + 4 * S::A_FLOATS;
+        unsigned char *bs = bx_area(slot);
         const int64_t u0 = (int64_t)s * RS;
         const int64_t rows_left = valid ? max64(0, min64(RS, w - u0)) : 0;
         const __amdgpu_buffer_rsrc_t b_rsrc = make_rsrc(p.Bc + u0 * n, (uint32_t)(rows_left * n * 4));
@@ -333,8 +373,7 @@ __global__ __launch_bounds__(T::NT) void nm_tiled_kernel(TiledArgs p)
     // each of this lane's compressed rows reads, per column group.
     int aoff[NKS][NCG];
     auto prep_offsets = [&](int slot) {
-        const int *Xs = reinterpret_cast<const int *>(lds + slot * S::SLOT_BYTES +
-                                                      4 * (S::A_FLOATS + S::B_FLOATS));
+        const int *Xs = reinterpret_cast<const int *>(bx_area(slot) + 4 * S::B_FLOATS);
 #pragma unroll
         for (int ks = 0; ks < NKS; ++ks)
 #pragma unroll
@@ -355,9 +394,10 @@ __global__ __launch_bounds__(T::NT) void nm_tiled_kernel(TiledArgs p)
     avec a[2][NCG][NRC];
     bvec b[2][NCG];
     auto fetch = [&](int slot, int ks, int sl) {
-        const unsigned char *base = lds + slot * S::SLOT_BYTES;
+        const unsigned char *base = a_area(slot);
         const unsigned char *Ab = base + (wm * WM + RPL * r) * 4;
-        const float *Bcol = reinterpret_cast<const float *>(base + 4 * S::A_FLOATS) + wn * WN + BV * r;
+        const float *Bcol = reinterpret_cast<const float *>(S::TWO_A ? base + S::A_BYTES : bx_area(slot)) +
+                            wn * WN + BV * r;
 #pragma unroll
         for (int cg = 0; cg < NCG; ++cg) {
 #pragma unroll
@@ -419,6 +459,8 @@ __global__ __launch_bounds__(T::NT) void nm_tiled_kernel(TiledArgs p)
                 dma_bx(s_begin + it + 1, cur ^ 1, next);
             }
         }
+        // one A_s slot: every wave must be done reading it
+        if constexpr (!S::TWO_A) lds_sync();
         store_a(cur ^ 1);
         stage_sync();
     }

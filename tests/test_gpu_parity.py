@@ -246,6 +246,36 @@ def test_every_tile_shape_exact(tile, shape, monkeypatch):
         f"{name}: {int(np.count_nonzero(C.astype(np.float64) != C_ref))} outputs differ"
 
 
+# Deep stages with one A_s slot (the tiles with at most 64 accumulators per
+# lane at KA = 128): ragged m / n, a last stage with fewer windows, split-k.
+ONE_A_TILES = ["128x256m32", "128x256", "256x128"]
+ONE_A = [
+    (300, 416, 544, 4, 32, 32),
+    (130, 640, 384, 2, 32, 32),
+    (260, 384, 288, 4, 32, 32),
+]
+
+
+@pytest.mark.parametrize("splits", [1, 2])
+@pytest.mark.parametrize("tile", ONE_A_TILES)
+@pytest.mark.parametrize("shape", ONE_A, ids=lambda s: "x".join(map(str, s)))
+def test_single_a_slot_deep_stages(tile, shape, splits, monkeypatch):
+    m, k, n, N, M, V = shape
+    monkeypatch.setenv("NMSPMM_TILE", tile)
+    monkeypatch.setenv("NMSPMM_KA", "128")
+    monkeypatch.setenv("NMSPMM_SPLITS", str(splits))
+    name = nm.nmspmm_kernel_name(m, n, k, N, M, V)
+    if tile == "128x256m32":
+        assert f"<{tile}," in name and ",ka128," in name, name
+    elif f"<{tile}," not in name or ",ka128," not in name:
+        pytest.skip(f"{tile} at KA = 128 does not fit {shape} ({name})")
+    C, C_ref, _ = parity(m, k, n, N, M, V, "int", seed=11 + m + n)
+    assert bool(np.array_equal(C.astype(np.float64), C_ref)), name
+    C, C_ref, Bnd = parity(m, k, n, N, M, V, "normal", seed=13 + m + n)
+    r = oracle.check(C, C_ref, Bnd)
+    assert r, (name, r)
+
+
 SKINNY = [
     (16, 2048, 640, 4, 32, 64),     # 2 chunks of A per split, ragged column tile
     (13, 3072, 384, 3, 8, 16),      # 3 chunks of 1024 columns, w not a multiple of 4
