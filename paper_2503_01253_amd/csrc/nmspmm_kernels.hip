@@ -99,6 +99,9 @@ const TileInfo TILES[] = {
     {"256x128", 256, 128, 16, 8, launch_tiled_256x128, tiled_fits_256x128},
     {"128x256m32", 128, 256, 32, 8, launch_tiled_128x256m32, tiled_fits_128x256m32},
     {"64x1024m32", 64, 1024, 32, 8, launch_tiled_64x1024m32, tiled_fits_64x1024m32},
+    {"256x256m32w16", 256, 256, 32, 16, launch_tiled_256x256m32w16, tiled_fits_256x256m32w16},
+    {"128x512m32w16", 128, 512, 32, 16, launch_tiled_128x512m32w16, tiled_fits_128x512m32w16},
+    {"128x256m32w16", 128, 256, 32, 16, launch_tiled_128x256m32w16, tiled_fits_128x256m32w16},
 };
 constexpr int NTILES = sizeof(TILES) / sizeof(TILES[0]);
 
@@ -152,13 +155,17 @@ bool tile_ok(const TileInfo &t, int BV, int KA, int NQ, int64_t k, int V)
 // CU when their stage is shallow, the others one.
 int acc_per_lane(const TileInfo &t) { return t.BM * t.BN / (64 * t.waves); }
 
+// 8-wave tiles with at most 64 accumulators per lane run two workgroups per
+// CU; 16-wave tiles (four waves per SIMD) run one.
+bool two_per_cu(const TileInfo &t) { return t.waves <= 8 && acc_per_lane(t) <= 64; }
+
 // Fraction of the workgroup slots a tile grid keeps busy over its waves of
 // workgroups (the last wave is usually partial), with slots = CUs x
 // workgroups per CU.
 double occupancy_of_grid(const TileInfo &t, int64_t m, int64_t n)
 {
     const int64_t tiles = ((m + t.BM - 1) / t.BM) * ((n + t.BN - 1) / t.BN);
-    const int64_t slots = 256 * (acc_per_lane(t) <= 64 ? 2 : 1);
+    const int64_t slots = 256 * (two_per_cu(t) ? 2 : 1);
     const int64_t rounds = (tiles + slots - 1) / slots;
     return (double)tiles / (double)(rounds * slots);
 }
@@ -168,12 +175,19 @@ double occupancy_of_grid(const TileInfo &t, int64_t m, int64_t n)
 //    tiles with split-k, which keep enough workgroups in flight to stream Bc;
 //  * m or n below 1024: the 128 x 256 tile with 32 x 32 MFMAs, else the
 //    128 x 128 tile (enough tiles to fill the chip, with split-k);
-//  * otherwise the 256 x 256 tile for dense-ish levels (N/M >= 1/2) and the
+//  * otherwise, at N/M <= 1/2 with V a multiple of 32, a 16-wave tile when
+//    its grid fills the chip in one round (at most 256 tiles, at least three
+//    quarters of the CUs busy): 256 x 256 at N/M = 1/2, 128 x 512 below,
+//    else 128 x 256.  Four waves per SIMD hide the A loads of one wave behind
+//    the MFMAs of the others (R2 566 -> 543 us, R3c 184 -> 163 us); on grids
+//    of several rounds (2048 x 11008) and on split-k grids the 8-wave tiles
+//    measured faster;
+//  * else the 256 x 256 tile for dense-ish levels (N/M >= 1/2) and the
 //    128 x 512 tile with 32 x 32 MFMAs for the sparser ones, unless its grid
 //    would leave more than a quarter of the chip idle in the last wave, where
-//    the 128 x 256 tile with 32 x 32 MFMAs (two workgroups per CU)
-//    quantises better.
-int preferences(int64_t m, int64_t n, int N, int M, const TileInfo **out)
+//    the 128 x 256 tile with 32 x 32 MFMAs (two workgroups per CU) is tried
+//    first.
+int preferences(int64_t m, int64_t n, int N, int M, int V, const TileInfo **out)
 {
     int c = 0;
     auto add = [&](const char *name) { out[c++] = tile_by_name(name); };
@@ -184,6 +198,16 @@ int preferences(int64_t m, int64_t n, int N, int M, const TileInfo **out)
     if (m < 1024 || n < 1024) {
         add("128x256m32"); add("128x128"); add("128x512"); add("256x256");
         return c;
+    }
+    if (2 * N <= M && V % 32 == 0) {
+        auto one_round = [&](const char *name) {
+            const TileInfo &t = *tile_by_name(name);
+            const int64_t tiles = ((m + t.BM - 1) / t.BM) * ((n + t.BN - 1) / t.BN);
+            return tiles <= 256 && occupancy_of_grid(t, m, n) >= 0.75;
+        };
+        const char *wide = 2 * N == M ? "256x256m32w16" : "128x512m32w16";
+        if (one_round(wide)) add(wide);
+        else if (one_round("128x256m32w16")) add("128x256m32w16");
     }
     const char *big = 2 * N >= M ? "256x256" : "128x512m32";
     if (occupancy_of_grid(*tile_by_name(big), m, n) < 0.75) add("128x256m32");
@@ -291,7 +315,7 @@ Plan make_plan(const float *A, const float *Bc, const float *C, int64_t m, int64
     }
 
     const TileInfo *cand[8];
-    int nc = preferences(m, n, N, M, cand);
+    int nc = preferences(m, n, N, M, V, cand);
     if (force_tile) {
         const TileInfo *t = tile_by_name(force_tile);
         if (t) { cand[0] = t; nc = 1; }
@@ -301,12 +325,14 @@ Plan make_plan(const float *A, const float *Bc, const float *C, int64_t m, int64
     int KA = 0, NQ = 0, BV = 0;
     for (int j = 0; j < nc && !tile; ++j) {
         if (!cand[j]) continue;
-        const int bv = bv_for(cand[j]->MI, V);
-        if (bv == 0 || !aligned(C, 4 * bv)) continue;
+      // the widest column group first; narrower ones where a wave's tile is
+      // narrower than MI * bv
+      for (int bv = bv_for(cand[j]->MI, V); bv >= 1 && !tile; bv /= 2) {
+        if (!aligned(C, 4 * bv)) continue;
         // the shallow rule pays off only when the grid has more tiles than
         // CUs, so that a second workgroup per CU has work to bring
         const int64_t tiles_c = ((m + cand[j]->BM - 1) / cand[j]->BM) * ((n + cand[j]->BN - 1) / cand[j]->BN);
-        const bool small = acc_per_lane(*cand[j]) <= 64 && tiles_c > 256;
+        const bool small = two_per_cu(*cand[j]) && tiles_c > 256;
         const int *order = small ? ka_small : ka_order;
         for (int i = 0; i < (small ? nks : nka) && !tile; ++i) {
             const int nq = stage_nq(order[i], (order[i] / M) * N);
@@ -317,6 +343,7 @@ Plan make_plan(const float *A, const float *Bc, const float *C, int64_t m, int64
                 BV = bv;
             }
         }
+      }
     }
     if (!tile) return p;
 

@@ -118,7 +118,11 @@ struct Shape {
     static constexpr int B_LANE = B_FLOATS * 4 / T::NT;
     static constexpr int B_W = B_LANE % 16 == 0 ? 16 : 4;
     static constexpr int B_CNT = B_LANE / B_W;
-    static constexpr bool FITS = (TWO_A || ONE_A_OK) && LDS_BYTES <= LDS_CAPACITY && KA % 32 == 0 &&
+    // 16-wave tiles run four waves per SIMD, 128 VGPRs each: one A staging
+    // chunk per wave and at most four quads per stage (more spill)
+    static constexpr bool REGS_OK = T::NT < 1024 || (NQ <= 4 && ACH == 1);
+    static constexpr bool FITS = (TWO_A || ONE_A_OK) && REGS_OK && LDS_BYTES <= LDS_CAPACITY &&
+                                 KA % 32 == 0 &&
                                  T::WN % CG == 0 && RST * QBMAX <= T::NT &&
                                  (B_FLOATS * 4) % T::NT == 0 && B_LANE % 4 == 0 && B_CNT >= 1;
 };

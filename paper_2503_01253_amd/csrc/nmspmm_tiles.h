@@ -25,6 +25,9 @@ NMSPMM_DECLARE_TILE(128x256)
 NMSPMM_DECLARE_TILE(256x128)
 NMSPMM_DECLARE_TILE(128x256m32)
 NMSPMM_DECLARE_TILE(64x1024m32)
+NMSPMM_DECLARE_TILE(256x256m32w16)
+NMSPMM_DECLARE_TILE(128x512m32w16)
+NMSPMM_DECLARE_TILE(128x256m32w16)
 
 #undef NMSPMM_DECLARE_TILE
 

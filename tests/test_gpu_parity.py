@@ -222,7 +222,7 @@ def test_out_of_range_offsets_stay_in_bounds():
 
 TILES = ["256x256", "128x512", "128x128", "64x512", "16x512", "128x256", "256x128",
          "256x256m32", "128x512m32", "128x128m32", "64x512m32", "128x256m32", "64x1024m32",
-         "skinny"]
+         "256x256m32w16", "128x512m32w16", "128x256m32w16", "skinny"]
 FORCED = [
     (300, 256, 1088, 8, 32, 32),
     (130, 384, 1024, 4, 32, 64),
@@ -248,7 +248,7 @@ def test_every_tile_shape_exact(tile, shape, monkeypatch):
 
 # Deep stages with one A_s slot (the tiles with at most 64 accumulators per
 # lane at KA = 128): ragged m / n, a last stage with fewer windows, split-k.
-ONE_A_TILES = ["128x256m32", "128x256", "256x128"]
+ONE_A_TILES = ["128x256m32", "128x256", "256x128", "128x256m32w16", "128x512m32w16"]
 ONE_A = [
     (300, 416, 544, 4, 32, 32),
     (130, 640, 384, 2, 32, 32),
@@ -265,7 +265,7 @@ def test_single_a_slot_deep_stages(tile, shape, splits, monkeypatch):
     monkeypatch.setenv("NMSPMM_KA", "128")
     monkeypatch.setenv("NMSPMM_SPLITS", str(splits))
     name = nm.nmspmm_kernel_name(m, n, k, N, M, V)
-    if tile == "128x256m32":
+    if tile in ("128x256m32", "128x256m32w16", "128x512m32w16"):
         assert f"<{tile}," in name and ",ka128," in name, name
     elif f"<{tile}," not in name or ",ka128," not in name:
         pytest.skip(f"{tile} at KA = 128 does not fit {shape} ({name})")
