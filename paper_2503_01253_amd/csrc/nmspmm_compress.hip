@@ -77,6 +77,7 @@ __global__ __launch_bounds__(PK_THREADS) void nm_compress_kernel(
 }
 
 constexpr int PK_LDS = 64 * 1024;   // LDS budget of the tiled packer
+constexpr int PK_BATCH = 8;          // staging loads in flight per thread
 
 // LDS layout of the tiled packer for bpw blocks: the tile (row stride
 // bpw * V + 1 floats, odd so that threads walking different rows of one
@@ -120,11 +121,24 @@ __global__ __launch_bounds__(PK_THREADS) void nm_compress_tile_kernel(
     const int64_t c0 = b0 * V;
     const int nrv = M * nb;   // row-vectors of this tile, index bl * M + o
 
-    // stage the tile: consecutive threads on consecutive columns
+    // stage the tile: consecutive threads on consecutive columns, PK_BATCH
+    // loads in flight per thread before their LDS writes
     const float *src = B + g * M * n + c0;
-    for (int e = t; e < M * cols; e += PK_THREADS) {
-        const int o = e / cols, c = e - o * cols;
-        tile[o * L.stride + c] = src[(int64_t)o * n + c];
+    const int total = M * cols;
+    for (int e0 = 0; e0 < total; e0 += PK_THREADS * PK_BATCH) {
+        float v[PK_BATCH];
+#pragma unroll
+        for (int i = 0; i < PK_BATCH; ++i) {
+            const int e = e0 + i * PK_THREADS + t;
+            const int o = e / cols, c = e - o * cols;
+            v[i] = e < total ? src[(int64_t)o * n + c] : 0.f;
+        }
+#pragma unroll
+        for (int i = 0; i < PK_BATCH; ++i) {
+            const int e = e0 + i * PK_THREADS + t;
+            const int o = e / cols, c = e - o * cols;
+            if (e < total) tile[o * L.stride + c] = v[i];
+        }
     }
     for (int e = t; e < N * nb; e += PK_THREADS) sel[e] = 0;
     __syncthreads();
