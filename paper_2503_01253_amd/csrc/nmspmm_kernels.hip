@@ -129,7 +129,7 @@ struct Plan {
     Kind kind = Kind::None;
     const TileInfo *tile = nullptr;
     int BV = 0, KA = 0, NQ = 0, RS = 0, stages = 0, splits = 1, tiles_m = 0, tiles_n = 0;
-    int QPW = 0, COLS = 0, CW = 0;   // streaming kernel only
+    int QPW = 0, COLS = 0, CW = 0, RT = 1;   // streaming kernel only
 };
 
 bool aligned(const void *p, int bytes) { return (reinterpret_cast<uintptr_t>(p) % bytes) == 0; }
@@ -253,12 +253,21 @@ bool plan_skinny(const float *A, const float *Bc, const float *C, int64_t m, int
 {
     if (V % 16 != 0 || M % 4 != 0) return false;
     if (!aligned(A, 16) || !aligned(Bc, 16) || !aligned(C, 16)) return false;
-    // buffer offsets: 16 rows of A and 4 rows of Bc per resource
-    if ((int64_t)skinny_rows() * k * 4 >= (int64_t(1) << 31)) return false;
+    // 32 rows per workgroup (Bc read once per 32 rows instead of 16) when
+    // that grid alone gives a workgroup per CU at 128 columns; measured on
+    // MI355X: 1024 x 2048 x 2048 at 4:32 41 -> 32 us, 512 x 2048 x 2048 at
+    // 8:32 30 -> 26 us.  Where the 32-row grid would need split-k it
+    // measured slower.
+    int rt = m >= 512 && ((m + 31) / 32) * ((n + 127) / 128) >= 256 ? 2 : 1;
+    const int fr = env_int("NMSPMM_RT", 0);
+    if (fr == 1 || fr == 2) rt = fr;
+    if (M > skinny_chunk_cols(rt)) return false;
+    // buffer offsets: the workgroup's rows of A and 4 rows of Bc per resource
+    if ((int64_t)skinny_rows(rt) * k * 4 >= (int64_t(1) << 31)) return false;
     if ((int64_t)4 * n * 4 >= (int64_t(1) << 31)) return false;
     // 256 columns per workgroup when that already gives a workgroup per CU,
     // else 128 (and split-k for the rest)
-    const int64_t tiles_m = (m + skinny_rows() - 1) / skinny_rows();
+    const int64_t tiles_m = (m + skinny_rows(rt) - 1) / skinny_rows(rt);
     int cols = tiles_m * ((n + 255) / 256) >= 256 ? 256 : 128;
     const int fc = env_int("NMSPMM_SKCOLS", 0);
     if (fc == 32 || fc == 64 || fc == 128 || fc == 256) cols = fc;
@@ -273,15 +282,16 @@ bool plan_skinny(const float *A, const float *Bc, const float *C, int64_t m, int
     const int fs = env_int("NMSPMM_SPLITS", 0);
     if (fs >= 1) splits = std::min<int64_t>(fs, std::max<int64_t>(G, 1));
     // longer runs per wave when each workgroup walks all of k
-    int qpw = splits == 1 && skinny_has(bv, 4, cols) ? 4 : skinny_has(bv, 2, cols) ? 2 : 1;
+    int qpw = splits == 1 && skinny_has(rt, bv, 4, cols) ? 4 : skinny_has(rt, bv, 2, cols) ? 2 : 1;
     const int fq = env_int("NMSPMM_QPW", 0);
-    if (skinny_has(bv, fq, cols)) qpw = fq;
-    if (!skinny_has(bv, qpw, cols) || ntiles * splits > INT32_MAX) return false;
+    if (skinny_has(rt, bv, fq, cols)) qpw = fq;
+    if (!skinny_has(rt, bv, qpw, cols) || ntiles * splits > INT32_MAX) return false;
     p.kind = Kind::Skinny;
     p.BV = bv;
     p.QPW = qpw;
     p.COLS = cols;
-    p.CW = skinny_chunk_cols() / M;
+    p.CW = skinny_chunk_cols(rt) / M;
+    p.RT = rt;
     p.splits = (int)splits;
     p.tiles_m = (int)tiles_m;
     p.tiles_n = (int)tiles_n;
@@ -435,7 +445,7 @@ hipError_t launch_main(const Plan &p, const float *A, const float *Bc, const uin
         s.tiles_n = p.tiles_n;
         s.cw = p.CW;
         s.epi = epi;
-        return launch_skinny(p.BV, p.QPW, p.COLS, s, stream);
+        return launch_skinny(p.RT, p.BV, p.QPW, p.COLS, s, stream);
     }
     TiledArgs a;
     a.A = A;
@@ -490,8 +500,12 @@ extern "C" const char *nmspmm_kernel_name(int64_t m, int64_t n, int64_t k, int N
     }
     thread_local char buf[96];
     if (p.kind == Kind::Skinny) {
-        std::snprintf(buf, sizeof buf, "nm_skinny_kernel<c%d,bv%d,qpw%d>%s%d", p.COLS, p.BV, p.QPW,
-                      p.splits > 1 ? "+zero,split" : ",split", p.splits);
+        if (p.RT == 1)
+            std::snprintf(buf, sizeof buf, "nm_skinny_kernel<c%d,bv%d,qpw%d>%s%d", p.COLS, p.BV, p.QPW,
+                          p.splits > 1 ? "+zero,split" : ",split", p.splits);
+        else
+            std::snprintf(buf, sizeof buf, "nm_skinny_kernel<c%d,bv%d,qpw%d,rows%d>%s%d", p.COLS, p.BV,
+                          p.QPW, 16 * p.RT, p.splits > 1 ? "+zero,split" : ",split", p.splits);
         return buf;
     }
     std::snprintf(buf, sizeof buf, "nm_tiled_kernel<%s,bv%d,ka%d,nq%d>%s%d", p.tile->name, p.BV,

@@ -19,18 +19,19 @@ struct SkinnyArgs {
     int N, M, V;
     int splits;          // workgroups per output tile along k (>1: atomic adds into a zeroed C)
     int tiles_m, tiles_n;
-    int cw;              // windows per staged chunk of A: cw * M <= skinny_chunk_cols()
+    int cw;              // windows per staged chunk of A: cw * M <= skinny_chunk_cols(RT)
     Epilogue epi;        // applied by the stores when splits == 1
 };
 
-int skinny_rows();        // rows of C per workgroup
-int skinny_chunk_cols();  // columns of A per staged chunk
+int skinny_rows(int RT);        // rows of C per workgroup with RT row tiles
+int skinny_chunk_cols(int RT);  // columns of A per staged chunk with RT row tiles
 
-// BV: columns per lane per B read (1, 2 or 4); QPW: quads per wave per round
-// (1, 2 or 4); COLS: columns of C per workgroup (32, 64, 128 or 256).  A must be
-// 16-byte aligned and M a multiple of 4 (16-byte loads of A along k).
-bool skinny_has(int BV, int QPW, int COLS);
-hipError_t launch_skinny(int BV, int QPW, int COLS, const SkinnyArgs &a, hipStream_t stream);
+// RT: row tiles of 16 rows per workgroup (1 or 2); BV: columns per lane per B
+// read (1, 2 or 4); QPW: quads per wave per round (1, 2, 4 or 8); COLS:
+// columns of C per workgroup (32, 64, 128 or 256).  A must be 16-byte aligned
+// and M a multiple of 4 (16-byte loads of A along k).
+bool skinny_has(int RT, int BV, int QPW, int COLS);
+hipError_t launch_skinny(int RT, int BV, int QPW, int COLS, const SkinnyArgs &a, hipStream_t stream);
 
 }  // namespace nmspmm
 

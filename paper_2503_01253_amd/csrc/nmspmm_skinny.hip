@@ -33,15 +33,22 @@ namespace nmspmm {
 
 namespace {
 
-constexpr int SK_ROWS = 16;     // rows of C per workgroup (one MFMA row tile)
 constexpr int SK_NW = 8;        // waves per workgroup
 constexpr int SK_NT = SK_NW * 64;
-constexpr int SK_KC = 1024;     // columns of A per chunk
-constexpr int SK_AS = SK_KC + 4;                  // LDS row stride of a chunk (floats)
-constexpr int SK_ABUF = SK_ROWS * SK_AS;          // floats per chunk buffer
+constexpr int SK_AREA = 16 * 1024;                // floats of A per chunk (rows x columns)
 constexpr int SK_SEG = 256;                       // floats per 16-byte DMA instruction (64 lanes)
-constexpr int SK_DMA = SK_ROWS * (SK_KC / SK_SEG) / SK_NW;   // DMA instructions per wave and chunk
-static_assert(SK_ROWS * (SK_KC / SK_SEG) % SK_NW == 0, "chunk DMA split");
+
+// Shape of a workgroup with RT row tiles of 16 rows: its A chunks hold
+// SK_AREA / ROWS columns, so that two of them fit in LDS at every RT.
+template <int RT>
+struct SkShape {
+    static constexpr int ROWS = 16 * RT;
+    static constexpr int KC = SK_AREA / ROWS;     // columns of A per chunk
+    static constexpr int AS = KC + 4;             // LDS row stride of a chunk (floats)
+    static constexpr int ABUF = ROWS * AS;        // floats per chunk buffer
+    static constexpr int DMA = ROWS * (KC / SK_SEG) / SK_NW;   // DMA instructions per wave and chunk
+    static_assert(KC % SK_SEG == 0 && ROWS * (KC / SK_SEG) % SK_NW == 0, "chunk DMA split");
+};
 
 // Workgroup barrier after all but the last VM global loads / DMA of this wave
 // have completed (vmcnt(VM), VM < 64) and its LDS accesses have too.
@@ -55,15 +62,23 @@ __device__ __forceinline__ void lds_barrier()
     asm volatile("" ::: "memory");
 }
 
-template <int BV, int QPW, int COLS>
+template <int RT, int BV, int QPW, int COLS>
 __global__ __launch_bounds__(SK_NT) void nm_skinny_kernel(SkinnyArgs p)
 {
+    using SS = SkShape<RT>;
+    constexpr int SK_ROWS = SS::ROWS, SK_KC = SS::KC, SK_AS = SS::AS, SK_ABUF = SS::ABUF;
+    constexpr int SK_DMA = SS::DMA;
     constexpr int CG = 16 * BV;             // columns per MFMA column group
     constexpr int NG = COLS / CG;           // column groups per workgroup
-    constexpr int RED = SK_NW * SK_ROWS * COLS;
-    constexpr int LDS_FLOATS = 2 * SK_ABUF > RED ? 2 * SK_ABUF : RED;
+    // the reduction sums the waves' partial tiles in SLOTS tiles of LDS,
+    // SK_NW / SLOTS waves deep
+    constexpr int TILE = SK_ROWS * COLS;
+    constexpr int LDS_FLOATS = 2 * SK_ABUF > TILE ? 2 * SK_ABUF : TILE;
+    constexpr int FIT = LDS_FLOATS / TILE;
+    constexpr int SLOTS = FIT >= 8 ? 8 : FIT >= 4 ? 4 : FIT >= 2 ? 2 : 1;
     constexpr int NL = 2 * QPW * NG;        // memory instructions per wave and round
     static_assert(SK_DMA + NL < 64, "vmcnt range");
+    static_assert(SK_NW % SLOTS == 0, "reduction passes");
     typedef typename vec_of<BV>::type bvec;
 
     // two A chunk buffers during the main loop; the reduction area after it
@@ -147,7 +162,10 @@ __global__ __launch_bounds__(SK_NT) void nm_skinny_kernel(SkinnyArgs p)
 #pragma unroll
             for (int g = 0; g < NG; ++g) {
                 const int64_t col = gcol[g] + BV * r;
-                const uint32_t boff = urow && col < n ? (uint32_t)((kq * n + col) * 4) : OOB;
+                // bit 31 (OOB) set unless the row and column exist: an offset
+                // past every buffer, without a branch (valid offsets are < 2^31)
+                const uint32_t boff = (uint32_t)((kq * n + col) * 4) |
+                                      ((uint32_t)!(urow && col < n) << 31);
                 // the buffer loads return raw dwords; reinterpret them as floats
                 if constexpr (BV == 4)
                     bv[j][g] = __builtin_bit_cast(
@@ -164,11 +182,13 @@ __global__ __launch_bounds__(SK_NT) void nm_skinny_kernel(SkinnyArgs p)
         }
     };
 
-    f32x4 acc[NG][BV];
+    f32x4 acc[RT][NG][BV];
 #pragma unroll
-    for (int g = 0; g < NG; ++g)
+    for (int t = 0; t < RT; ++t)
 #pragma unroll
-        for (int s = 0; s < BV; ++s) acc[g][s] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int g = 0; g < NG; ++g)
+#pragma unroll
+            for (int s = 0; s < BV; ++s) acc[t][g][s] = f32x4{0.f, 0.f, 0.f, 0.f};
 
     // ---- gather A from the chunk in `buf`, MFMAs ----
     auto compute = [&](int buf, int64_t u0, int64_t u1, int rd, const bvec (&bv)[QPW][NG],
@@ -181,11 +201,16 @@ __global__ __launch_bounds__(SK_NT) void nm_skinny_kernel(SkinnyArgs p)
             const int wbase = u < u1 ? (int)(((uint32_t)(u - u0) * invN) >> 20) * M : 0;
 #pragma unroll
             for (int g = 0; g < NG; ++g) {
-                const float a = As[wbase + min(off[j][g], M - 1)];
+                const int ac = wbase + min(off[j][g], M - 1);
+                // one Bc operand feeds the MFMAs of every row tile
 #pragma unroll
-                for (int s = 0; s < BV; ++s)
-                    acc[g][s] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, lane_of<BV>(bv[j][g], s),
-                                                                     acc[g][s], 0, 0, 0);
+                for (int t = 0; t < RT; ++t) {
+                    const float a = As[t * 16 * SK_AS + ac];
+#pragma unroll
+                    for (int s = 0; s < BV; ++s)
+                        acc[t][g][s] = __builtin_amdgcn_mfma_f32_16x16x4f32(
+                            a, lane_of<BV>(bv[j][g], s), acc[t][g][s], 0, 0, 0);
+                }
             }
         }
     };
@@ -193,8 +218,8 @@ __global__ __launch_bounds__(SK_NT) void nm_skinny_kernel(SkinnyArgs p)
     // ---- chunk loop.  Memory instructions in flight at the barrier that
     // opens chunk c, newest first: the loads of round 0 of chunk c (NL), the
     // DMA of chunk c+1 (SK_DMA); everything older, chunk c's DMA included,
-    // must be done.  (Loading round r+1 while round r is multiplied measured
-    // slower: the handover of the operand registers waits for the loads.) ----
+    // must be done.  (Loading the next round, or the next chunk's round,
+    // while one is multiplied measured no faster on MI355X.) ----
     bvec bv[QPW][NG];
     int off[QPW][NG];
     if (nchunks > 0) {
@@ -219,31 +244,42 @@ __global__ __launch_bounds__(SK_NT) void nm_skinny_kernel(SkinnyArgs p)
     lds_barrier<0>();
 
     // ---- sum the waves' partial tiles through LDS (fixed order) ----
-    // lane l holds rows 4*(l/16)+e, columns g*CG + BV*(l%16)+s
-    float *mine = lds + wave * SK_ROWS * COLS;
+    // lane l holds rows 16*t + 4*(l/16)+e, columns g*CG + BV*(l%16)+s.  In
+    // pass i, waves i*SLOTS .. i*SLOTS+SLOTS-1 write (i == 0) or add (i > 0)
+    // their tiles into slots 0 .. SLOTS-1.
 #pragma unroll
-    for (int g = 0; g < NG; ++g)
+    for (int pass = 0; pass < SK_NW / SLOTS; ++pass) {
+        if (wave / SLOTS == pass) {
+            float *mine = lds + (wave % SLOTS) * TILE;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            bvec v;
-            if constexpr (BV == 1) {
-                v = acc[g][0][e];
-            } else {
+            for (int t = 0; t < RT; ++t)
 #pragma unroll
-                for (int s = 0; s < BV; ++s) v[s] = acc[g][s][e];
-            }
-            *reinterpret_cast<bvec *>(mine + (4 * kq + e) * COLS + g * CG + BV * r) = v;
+                for (int g = 0; g < NG; ++g)
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        bvec v;
+                        if constexpr (BV == 1) {
+                            v = acc[t][g][0][e];
+                        } else {
+#pragma unroll
+                            for (int s = 0; s < BV; ++s) v[s] = acc[t][g][s][e];
+                        }
+                        bvec *dst = reinterpret_cast<bvec *>(mine + (16 * t + 4 * kq + e) * COLS +
+                                                             g * CG + BV * r);
+                        if (pass == 0) *dst = v;
+                        else *dst += v;
+                    }
         }
-    lds_barrier<0>();
+        lds_barrier<0>();
+    }
     // one output per lane and step, consecutive lanes on consecutive columns
     // (coalesced stores and atomics)
-    constexpr int OUT = SK_ROWS * COLS;
-    static_assert(OUT % SK_NT == 0, "reduction split");
+    static_assert(TILE % SK_NT == 0, "reduction split");
 #pragma unroll
-    for (int e = tid; e < OUT; e += SK_NT) {
+    for (int e = tid; e < TILE; e += SK_NT) {
         float sum = lds[e];
 #pragma unroll
-        for (int wv = 1; wv < SK_NW; ++wv) sum += lds[wv * OUT + e];
+        for (int sl = 1; sl < SLOTS; ++sl) sum += lds[sl * TILE + e];
         const int64_t row = row0 + e / COLS, col = col0 + e % COLS;
         if (row >= m || col >= n) continue;
         if (p.splits == 1)
@@ -253,42 +289,44 @@ __global__ __launch_bounds__(SK_NT) void nm_skinny_kernel(SkinnyArgs p)
     }
 }
 
-template <int BV, int QPW, int COLS>
+template <int RT, int BV, int QPW, int COLS>
 hipError_t launch(const SkinnyArgs &a, hipStream_t stream)
 {
     const unsigned grid = (unsigned)a.tiles_m * (unsigned)a.tiles_n * (unsigned)a.splits;
-    hipLaunchKernelGGL((nm_skinny_kernel<BV, QPW, COLS>), dim3(grid), dim3(SK_NT), 0, stream, a);
+    hipLaunchKernelGGL((nm_skinny_kernel<RT, BV, QPW, COLS>), dim3(grid), dim3(SK_NT), 0, stream, a);
     return hipGetLastError();
 }
 
 }  // namespace
 
-int skinny_rows() { return SK_ROWS; }
-int skinny_chunk_cols() { return SK_KC; }
+int skinny_rows(int RT) { return 16 * RT; }
+int skinny_chunk_cols(int RT) { return SK_AREA / (16 * RT); }
 
-// Instantiated (BV, QPW, COLS): the ones that fit in registers without
+// Instantiated (RT, BV, QPW, COLS): the ones that fit in registers without
 // spills, with BV * 16 <= COLS.
-#define NMSPMM_SKINNY_VARIANTS(X)                                                    \
-    X(1, 1, 32) X(1, 2, 32) X(1, 4, 32) X(1, 8, 32) X(2, 1, 32) X(2, 2, 32) X(2, 4, 32) \
-    X(2, 8, 32) X(1, 1, 64) X(1, 2, 64) X(1, 4, 64) X(2, 1, 64) X(2, 2, 64) X(2, 4, 64) \
-    X(4, 1, 64) X(4, 2, 64) X(4, 4, 64) X(4, 8, 64)                                  \
-    X(1, 1, 128) X(1, 2, 128) X(2, 1, 128) X(2, 2, 128) X(2, 4, 128)                 \
-    X(4, 1, 128) X(4, 2, 128) X(4, 4, 128)                                           \
-    X(1, 1, 256) X(2, 1, 256) X(2, 2, 256) X(4, 1, 256) X(4, 2, 256)
+#define NMSPMM_SKINNY_VARIANTS(X)                                                              \
+    X(1, 1, 1, 32) X(1, 1, 2, 32) X(1, 1, 4, 32) X(1, 1, 8, 32) X(1, 2, 1, 32) X(1, 2, 2, 32)   \
+    X(1, 2, 4, 32) X(1, 2, 8, 32) X(1, 1, 1, 64) X(1, 1, 2, 64) X(1, 1, 4, 64) X(1, 2, 1, 64)   \
+    X(1, 2, 2, 64) X(1, 2, 4, 64) X(1, 4, 1, 64) X(1, 4, 2, 64) X(1, 4, 4, 64) X(1, 4, 8, 64)   \
+    X(1, 1, 1, 128) X(1, 1, 2, 128) X(1, 2, 1, 128) X(1, 2, 2, 128) X(1, 2, 4, 128)            \
+    X(1, 4, 1, 128) X(1, 4, 2, 128) X(1, 4, 4, 128)                                            \
+    X(1, 1, 1, 256) X(1, 2, 1, 256) X(1, 2, 2, 256) X(1, 4, 1, 256) X(1, 4, 2, 256)            \
+    X(2, 2, 1, 128) X(2, 2, 2, 128) X(2, 4, 1, 128) X(2, 4, 2, 128) X(2, 4, 4, 128)            \
+    X(2, 2, 1, 256) X(2, 2, 2, 256) X(2, 4, 1, 256)
 
-bool skinny_has(int BV, int QPW, int COLS)
+bool skinny_has(int RT, int BV, int QPW, int COLS)
 {
-#define NM_SK_HAS(bv, qpw, cols) \
-    if (BV == bv && QPW == qpw && COLS == cols) return true;
+#define NM_SK_HAS(rt, bv, qpw, cols) \
+    if (RT == rt && BV == bv && QPW == qpw && COLS == cols) return true;
     NMSPMM_SKINNY_VARIANTS(NM_SK_HAS)
 #undef NM_SK_HAS
     return false;
 }
 
-hipError_t launch_skinny(int BV, int QPW, int COLS, const SkinnyArgs &a, hipStream_t stream)
+hipError_t launch_skinny(int RT, int BV, int QPW, int COLS, const SkinnyArgs &a, hipStream_t stream)
 {
-#define NM_SK_LAUNCH(bv, qpw, cols) \
-    if (BV == bv && QPW == qpw && COLS == cols) return launch<bv, qpw, cols>(a, stream);
+#define NM_SK_LAUNCH(rt, bv, qpw, cols) \
+    if (RT == rt && BV == bv && QPW == qpw && COLS == cols) return launch<rt, bv, qpw, cols>(a, stream);
     NMSPMM_SKINNY_VARIANTS(NM_SK_LAUNCH)
 #undef NM_SK_LAUNCH
     return hipErrorInvalidValue;

@@ -305,6 +305,47 @@ def test_skinny_variants_exact(shape, splits, cols, qpw, monkeypatch):
         f"{name}: {int(np.count_nonzero(C.astype(np.float64) != C_ref))} outputs differ"
 
 
+# 32-row workgroups (two row tiles share each Bc operand): rows past m in the
+# second tile, several chunks, M = 8 and M = 256 windows, split-k
+SKINNY32 = [
+    (40, 1536, 256, 8, 32, 32),
+    (100, 1024, 640, 4, 32, 64),
+    (64, 2048, 512, 3, 8, 32),
+    (30, 1024, 256, 5, 256, 64),
+]
+
+
+@pytest.mark.parametrize("cols,qpw", [(128, 1), (128, 2), (128, 4), (256, 1), (256, 2)])
+@pytest.mark.parametrize("splits", [1, 3])
+@pytest.mark.parametrize("shape", SKINNY32, ids=lambda s: "x".join(map(str, s)))
+def test_skinny_32_row_variants_exact(shape, splits, cols, qpw, monkeypatch):
+    """The streaming kernel with 32 rows per workgroup, forced, on
+    small-integer data (exact in any summation order), and on normal data
+    against the bar."""
+    m, k, n, N, M, V = shape
+    monkeypatch.setenv("NMSPMM_TILE", "skinny")
+    monkeypatch.setenv("NMSPMM_RT", "2")
+    monkeypatch.setenv("NMSPMM_SKCOLS", str(cols))
+    monkeypatch.setenv("NMSPMM_QPW", str(qpw))
+    monkeypatch.setenv("NMSPMM_SPLITS", str(splits))
+    name = nm.nmspmm_kernel_name(m, n, k, N, M, V)
+    if not name.startswith(f"nm_skinny_kernel<c{cols},") or f"qpw{qpw},rows32>" not in name:
+        pytest.skip(f"variant not instantiated for {shape} ({name})")
+    C, C_ref, _ = parity(m, k, n, N, M, V, "int", seed=21 + m + n)
+    assert bool(np.array_equal(C.astype(np.float64), C_ref)), \
+        f"{name}: {int(np.count_nonzero(C.astype(np.float64) != C_ref))} outputs differ"
+    C, C_ref, Bnd = parity(m, k, n, N, M, V, "normal", seed=23 + m + n)
+    r = oracle.check(C, C_ref, Bnd)
+    assert r, (name, r)
+
+
+def test_skinny_32_rows_chosen_for_wide_grids():
+    """The dispatcher takes 32-row workgroups where that grid alone fills the
+    chip (512 x 2048 x 2048 at 4:32), and 16 rows for decode-like shapes."""
+    assert nm.nmspmm_kernel_name(512, 2048, 2048, 4, 32, 32).endswith("rows32>,split1")
+    assert "rows32" not in nm.nmspmm_kernel_name(64, 8192, 8192, 4, 32, 64)
+
+
 def test_dense_comparator_is_true_fp32():
     """The benchmark's dense comparator (torch.matmul on the decompressed B,
     TF32 off) meets the same bar, so it is a true fp32 GEMM."""
