@@ -264,7 +264,8 @@ bool plan_skinny(const float *A, const float *Bc, const float *C, int64_t m, int
     if (M > skinny_chunk_cols(rt)) return false;
     // buffer offsets: the workgroup's rows of A and 4 rows of Bc per resource
     if ((int64_t)skinny_rows(rt) * k * 4 >= (int64_t(1) << 31)) return false;
-    if ((int64_t)4 * n * 4 >= (int64_t(1) << 31)) return false;
+    // Bc byte offsets inside a chunk (at most 1024 rows, plus a quad)
+    if ((int64_t)1028 * n * 4 >= (int64_t(1) << 31)) return false;
     // 256 columns per workgroup when that already gives a workgroup per CU,
     // else 128 (and split-k for the rest)
     const int64_t tiles_m = (m + skinny_rows(rt) - 1) / skinny_rows(rt);

@@ -146,38 +146,46 @@ __global__ __launch_bounds__(SK_NT) void nm_skinny_kernel(SkinnyArgs p)
         u1 = min64(ge, w0 + cw) * N;
     };
 
+    // Per lane and column group, fixed for the whole kernel: the byte offset
+    // of its Bc values and of its offset byte relative to a quad's first
+    // compressed row (row kq of the quad).  Bc offsets past the last column
+    // get bit 31 (OOB), an offset past every buffer (valid ones stay below
+    // 2^31 after the row offset is added: the host keeps 1028 * n * 4 under
+    // 2^31).
+    uint32_t boff[NG], xoff[NG];
+#pragma unroll
+    for (int g = 0; g < NG; ++g) {
+        const int64_t col = gcol[g] + BV * r;
+        boff[g] = (uint32_t)((kq * n + col) * 4) | ((uint32_t)!(col < n) << 31);
+        xoff[g] = (uint32_t)(kq * q + gblk[g]);
+    }
+
     // ---- one round's Bc operands and offsets, straight into registers ----
+    // One resource per chunk for its Bc rows and one for their offset bytes:
+    // rows past the chunk fall outside them and read zero.  (Building the
+    // resources per quad kept the scalar unit busier than the matrix pipe.)
     auto load_round = [&](int64_t c, int rd, bvec (&bv)[QPW][NG], int (&off)[QPW][NG]) {
         int64_t u0, u1;
         chunk_rows(c, u0, u1);
-        const int64_t ub = u0 + ((int64_t)rd * SK_NW + wave) * QPW * 4;
+        const int64_t nrows = max64(0, u1 - u0);
+        const __amdgpu_buffer_rsrc_t b_rsrc = make_rsrc(p.Bc + u0 * n, (uint32_t)(nrows * n * 4));
+        const __amdgpu_buffer_rsrc_t x_rsrc = make_rsrc(p.idx + u0 * q, (uint32_t)(nrows * q));
+        const uint32_t rb = (uint32_t)((rd * SK_NW + wave) * QPW * 4);   // chunk-relative
 #pragma unroll
         for (int j = 0; j < QPW; ++j) {
-            const int64_t rows_left = max64(0, u1 - (ub + 4 * j));
-            const __amdgpu_buffer_rsrc_t b_rsrc =
-                make_rsrc(p.Bc + (ub + 4 * j) * n,
-                          (uint32_t)(min64(rows_left, 4) * n * 4));
-            const int64_t u = ub + 4 * j + kq;
-            const bool urow = u < u1;
+            const uint32_t rj = rb + 4 * j;                // the quad's first row
+            const uint32_t brow = rj * (uint32_t)n * 4, xrow = rj * (uint32_t)q;
 #pragma unroll
             for (int g = 0; g < NG; ++g) {
-                const int64_t col = gcol[g] + BV * r;
-                // bit 31 (OOB) set unless the row and column exist: an offset
-                // past every buffer, without a branch (valid offsets are < 2^31)
-                const uint32_t boff = (uint32_t)((kq * n + col) * 4) |
-                                      ((uint32_t)!(urow && col < n) << 31);
+                const int bo = (int)(boff[g] + brow);
                 // the buffer loads return raw dwords; reinterpret them as floats
                 if constexpr (BV == 4)
-                    bv[j][g] = __builtin_bit_cast(
-                        f32x4, __builtin_amdgcn_raw_buffer_load_b128(b_rsrc, (int)boff, 0, 0));
+                    bv[j][g] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(b_rsrc, bo, 0, 0));
                 else if constexpr (BV == 2)
-                    bv[j][g] = __builtin_bit_cast(
-                        f32x2, __builtin_amdgcn_raw_buffer_load_b64(b_rsrc, (int)boff, 0, 0));
+                    bv[j][g] = __builtin_bit_cast(f32x2, __builtin_amdgcn_raw_buffer_load_b64(b_rsrc, bo, 0, 0));
                 else
-                    bv[j][g] = __builtin_bit_cast(
-                        float, __builtin_amdgcn_raw_buffer_load_b32(b_rsrc, (int)boff, 0, 0));
-                const bool ok = urow && gcol[g] < n;
-                off[j][g] = p.idx[ok ? u * q + gblk[g] : 0];
+                    bv[j][g] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(b_rsrc, bo, 0, 0));
+                off[j][g] = __builtin_amdgcn_raw_buffer_load_b8(x_rsrc, (int)(xoff[g] + xrow), 0, 0);
             }
         }
     };
@@ -194,11 +202,13 @@ __global__ __launch_bounds__(SK_NT) void nm_skinny_kernel(SkinnyArgs p)
     auto compute = [&](int buf, int64_t u0, int64_t u1, int rd, const bvec (&bv)[QPW][NG],
                        const int (&off)[QPW][NG]) {
         const float *As = lds + buf * SK_ABUF + r * SK_AS;
-        const int64_t ub = u0 + ((int64_t)rd * SK_NW + wave) * QPW * 4;
+        // row indices relative to the chunk (fewer than 1024 rows)
+        const int nrows = (int)max64(0, u1 - u0);
+        const int rb = (rd * SK_NW + wave) * QPW * 4 + kq;
 #pragma unroll
         for (int j = 0; j < QPW; ++j) {
-            const int64_t u = ub + 4 * j + kq;
-            const int wbase = u < u1 ? (int)(((uint32_t)(u - u0) * invN) >> 20) * M : 0;
+            const int ur = rb + 4 * j;
+            const int wbase = ur < nrows ? (int)(((uint32_t)ur * invN) >> 20) * M : 0;
 #pragma unroll
             for (int g = 0; g < NG; ++g) {
                 const int ac = wbase + min(off[j][g], M - 1);
