@@ -16,6 +16,7 @@
 #include "nmspmm.h"
 #include "nmspmm_internal.h"
 #include "nmspmm_skinny.h"
+#include "nmspmm_stream.h"
 #include "nmspmm_tiled.h"
 #include "nmspmm_tiles.h"
 
@@ -123,13 +124,14 @@ const TileInfo *tile_by_name(const char *name)
     return nullptr;
 }
 
-enum class Kind { None, General, Tiled, Skinny };
+enum class Kind { None, General, Tiled, Skinny, Stream };
 
 struct Plan {
     Kind kind = Kind::None;
     const TileInfo *tile = nullptr;
     int BV = 0, KA = 0, NQ = 0, RS = 0, stages = 0, splits = 1, tiles_m = 0, tiles_n = 0;
-    int QPW = 0, COLS = 0, CW = 0, RT = 1;   // streaming kernel only
+    int QPW = 0, COLS = 0, CW = 0, RT = 1;   // streaming kernels only
+    int CPW = 0, RB = 0, SW = 0;             // pipelined streaming kernel only
 };
 
 bool aligned(const void *p, int bytes) { return (reinterpret_cast<uintptr_t>(p) % bytes) == 0; }
@@ -299,6 +301,87 @@ bool plan_skinny(const float *A, const float *Bc, const float *C, int64_t m, int
     return true;
 }
 
+// Pipelined streaming kernel: loader waves stream A, Bc and the offsets into
+// an LDS ring several stages ahead of the compute waves.  Measured on MI355X
+// against the register-operand streaming kernel: 64 x 8192 x 8192 at 4:32
+// 29.1 -> 26.6 us, 128 x 8192 x 8192 42.5 -> 39.1, 1024 x 2048 x 2048 32.9 ->
+// 20.4, 512 x 2048 x 2048 18.6 -> 15.3, 512 x 512 x 512 9.6 -> 7.0; at 8:32
+// 512 x 2048 x 2048 24.3 -> 21.7.  It loses at 16 rows (the 16-row decode
+// shapes keep the other kernel) and gains nothing at the denser levels.
+// `force` (tuning sweeps and tests) takes it wherever it can run.
+bool plan_stream(const float *A, const float *Bc, const float *C, int64_t m, int64_t n, int64_t k,
+                 int N, int M, int V, bool force, Plan &p)
+{
+    const int KS = stream_stage_cols();
+    if (V % 16 != 0 || M % 4 != 0 || M > KS) return false;
+    if (!aligned(A, 16) || !aligned(Bc, 16) || !aligned(C, 16)) return false;
+    // compressed rows per stage: the smallest ring row count that holds a
+    // whole stage of KS/M windows, else the largest
+    int rb = 64;
+    for (int r : {16, 32, 64})
+        if ((KS / M) * N <= r) { rb = r; break; }
+    const int frb = env_int("NMSPMM_PSRB", 0);
+    if (frb == 16 || frb == 32 || frb == 64) rb = frb;
+    if (N > rb) return false;
+    if (!force && (rb > 32 || m <= 16)) return false;
+    const int sw = std::min(KS / M, rb / N);
+    const int64_t G = k / M;
+    const int64_t nstages = (G + sw - 1) / sw;
+    const int bvmax = std::min(bv_for(16, V), 2);
+    auto ntiles = [&](int rt, int bv) {
+        return ((m + stream_rows(rt) - 1) / stream_rows(rt)) * ((n + stream_cols(bv, 1) - 1) / stream_cols(bv, 1));
+    };
+    // Short products: 32-row tiles, k split until about one workgroup per
+    // CU.  Taller ones: the largest tile whose grid alone fills the chip,
+    // else the smallest, without split-k (their k is short: splitting it
+    // measured slower).
+    int rt = 2, bv = bvmax;
+    bool fill_splits = m <= 128;
+    if (m > 128) {
+        const int order[][2] = {{2, 2}, {1, 2}, {1, 1}};
+        rt = 1;
+        bv = 1;
+        for (const auto &o : order)
+            if (o[1] <= bvmax && ntiles(o[0], o[1]) >= 256) {
+                rt = o[0];
+                bv = o[1];
+                break;
+            }
+    }
+    const int frt = env_int("NMSPMM_PSRT", 0);
+    if (frt == 1 || frt == 2 || frt == 4) rt = frt;
+    const int fbv = env_int("NMSPMM_PSBV", 0);
+    if ((fbv == 1 || fbv == 2 || fbv == 4) && V % (16 * fbv) == 0) bv = fbv;
+    int cpw = 1;
+    const int fcp = env_int("NMSPMM_PSCPW", 0);
+    if (fcp == 1 || fcp == 2) cpw = fcp;
+    if (!stream_has(rt, bv, cpw, rb)) return false;
+    if ((int64_t)stream_rows(rt) * k * 4 >= (int64_t(1) << 31)) return false;
+    if ((int64_t)rb * n * 4 >= (int64_t(1) << 31)) return false;
+    const int cols = stream_cols(bv, cpw);
+    const int64_t tiles_m = (m + stream_rows(rt) - 1) / stream_rows(rt);
+    const int64_t tiles_n = (n + cols - 1) / cols;
+    if (tiles_m * tiles_n > (1 << 24)) return false;
+    const int64_t tiles = tiles_m * tiles_n;
+    int64_t splits = 1;
+    if (fill_splits)   // at least two stages per workgroup
+        splits = std::max<int64_t>(1, std::min<int64_t>({(256 + tiles - 1) / tiles, nstages / 2, 64}));
+    const int fs = env_int("NMSPMM_SPLITS", 0);
+    if (fs >= 1) splits = std::min<int64_t>(fs, std::max<int64_t>(G, 1));
+    if (tiles * splits > INT32_MAX) return false;
+    p.kind = Kind::Stream;
+    p.RT = rt;
+    p.BV = bv;
+    p.CPW = cpw;
+    p.RB = rb;
+    p.SW = sw;
+    p.COLS = cols;
+    p.splits = (int)splits;
+    p.tiles_m = (int)tiles_m;
+    p.tiles_n = (int)tiles_n;
+    return true;
+}
+
 Plan make_plan(const float *A, const float *Bc, const float *C, int64_t m, int64_t n, int64_t k,
                int N, int M, int V)
 {
@@ -307,7 +390,13 @@ Plan make_plan(const float *A, const float *Bc, const float *C, int64_t m, int64
     const char *force_tile = std::getenv("NMSPMM_TILE");  // tuning sweeps only
     const bool want_skinny =
         force_tile ? std::strcmp(force_tile, "skinny") == 0 : prefer_streaming(m, k, N, M);
-    if (want_skinny && plan_skinny(A, Bc, C, m, n, k, N, M, V, p)) return p;
+    if (want_skinny) {
+        // NMSPMM_PS (tuning sweeps and tests): 0 never takes the pipelined
+        // streaming kernel, 1 takes it wherever it can run
+        const int ps = env_int("NMSPMM_PS", -1);
+        if (ps != 0 && plan_stream(A, Bc, C, m, n, k, N, M, V, ps == 1, p)) return p;
+        if (plan_skinny(A, Bc, C, m, n, k, N, M, V, p)) return p;
+    }
     p.kind = Kind::General;
     if (k % 4 != 0 || V % 16 != 0 || 128 % M != 0) return p;
     if (!aligned(A, 16) || !aligned(Bc, 16)) return p;
@@ -448,6 +537,25 @@ hipError_t launch_main(const Plan &p, const float *A, const float *Bc, const uin
         s.epi = epi;
         return launch_skinny(p.RT, p.BV, p.QPW, p.COLS, s, stream);
     }
+    if (p.kind == Kind::Stream) {
+        StreamArgs s;
+        s.A = A;
+        s.Bc = Bc;
+        s.idx = idx;
+        s.C = C;
+        s.m = m;
+        s.n = n;
+        s.k = k;
+        s.N = N;
+        s.M = M;
+        s.V = V;
+        s.splits = p.splits;
+        s.tiles_m = p.tiles_m;
+        s.tiles_n = p.tiles_n;
+        s.sw = p.SW;
+        s.epi = epi;
+        return launch_stream(p.RT, p.BV, p.CPW, p.RB, s, stream);
+    }
     TiledArgs a;
     a.A = A;
     a.Bc = Bc;
@@ -497,9 +605,14 @@ extern "C" const char *nmspmm_kernel_name(int64_t m, int64_t n, int64_t k, int N
     switch (p.kind) {
     case Kind::None: return "none";
     case Kind::General: return "nm_general_kernel";
-    case Kind::Tiled: case Kind::Skinny: break;
+    case Kind::Tiled: case Kind::Skinny: case Kind::Stream: break;
     }
     thread_local char buf[96];
+    if (p.kind == Kind::Stream) {
+        std::snprintf(buf, sizeof buf, "nm_stream_kernel<r%d,c%d,bv%d,rb%d>%s%d", 16 * p.RT, p.COLS,
+                      p.BV, p.RB, p.splits > 1 ? "+zero,split" : ",split", p.splits);
+        return buf;
+    }
     if (p.kind == Kind::Skinny) {
         if (p.RT == 1)
             std::snprintf(buf, sizeof buf, "nm_skinny_kernel<c%d,bv%d,qpw%d>%s%d", p.COLS, p.BV, p.QPW,

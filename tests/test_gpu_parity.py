@@ -294,6 +294,7 @@ def test_skinny_variants_exact(shape, splits, cols, qpw, monkeypatch):
     k split), forced, on small-integer data (exact in any summation order)."""
     m, k, n, N, M, V = shape
     monkeypatch.setenv("NMSPMM_TILE", "skinny")
+    monkeypatch.setenv("NMSPMM_PS", "0")
     monkeypatch.setenv("NMSPMM_SKCOLS", str(cols))
     monkeypatch.setenv("NMSPMM_QPW", str(qpw))
     monkeypatch.setenv("NMSPMM_SPLITS", str(splits))
@@ -324,6 +325,7 @@ def test_skinny_32_row_variants_exact(shape, splits, cols, qpw, monkeypatch):
     against the bar."""
     m, k, n, N, M, V = shape
     monkeypatch.setenv("NMSPMM_TILE", "skinny")
+    monkeypatch.setenv("NMSPMM_PS", "0")
     monkeypatch.setenv("NMSPMM_RT", "2")
     monkeypatch.setenv("NMSPMM_SKCOLS", str(cols))
     monkeypatch.setenv("NMSPMM_QPW", str(qpw))
@@ -339,11 +341,72 @@ def test_skinny_32_row_variants_exact(shape, splits, cols, qpw, monkeypatch):
     assert r, (name, r)
 
 
-def test_skinny_32_rows_chosen_for_wide_grids():
-    """The dispatcher takes 32-row workgroups where that grid alone fills the
-    chip (512 x 2048 x 2048 at 4:32), and 16 rows for decode-like shapes."""
+def test_skinny_32_rows_chosen_for_wide_grids(monkeypatch):
+    """Without the pipelined kernel, the register-operand streaming kernel
+    takes 32-row workgroups where that grid alone fills the chip (512 x 2048
+    x 2048 at 4:32), and 16 rows for decode-like shapes."""
+    monkeypatch.setenv("NMSPMM_PS", "0")
     assert nm.nmspmm_kernel_name(512, 2048, 2048, 4, 32, 32).endswith("rows32>,split1")
     assert "rows32" not in nm.nmspmm_kernel_name(64, 8192, 8192, 4, 32, 64)
+
+
+# ---- pipelined streaming kernel (loader waves, LDS ring) ----
+# ragged rows (rows past m in 32- and 64-row tiles), ragged column tiles,
+# partial last stages, stages that hold fewer rows than the ring (N = 1, 3,
+# 5), M = 8 / 16 / 32 / 64 / 128, V = 16 / 32 / 64, and k splits that leave
+# some workgroups without a window
+STREAM = [
+    (40, 1536, 512, 4, 32, 64),
+    (70, 1000, 832, 3, 8, 64),
+    (33, 2048, 320, 5, 64, 32),
+    (100, 512, 768, 4, 16, 16),
+    (16, 4096, 256, 1, 128, 64),
+    (20, 64, 256, 4, 32, 64),
+]
+STREAM_VARIANTS = [(1, 1, 1, 16), (1, 2, 1, 16), (1, 4, 1, 16), (1, 2, 1, 32), (1, 4, 1, 32),
+                   (1, 1, 1, 64), (2, 1, 1, 16), (2, 2, 1, 16), (2, 4, 1, 16), (2, 2, 1, 32),
+                   (2, 1, 1, 32), (4, 1, 1, 16), (4, 2, 1, 16), (2, 2, 2, 16), (1, 2, 2, 16)]
+
+
+@pytest.mark.parametrize("splits", [1, 3])
+@pytest.mark.parametrize("variant", STREAM_VARIANTS, ids=lambda v: "rt%d_bv%d_cpw%d_rb%d" % v)
+@pytest.mark.parametrize("shape", STREAM, ids=lambda s: "x".join(map(str, s)))
+def test_stream_variants_exact(shape, variant, splits, monkeypatch):
+    """Every instantiation of the pipelined streaming kernel (row tiles,
+    columns per lane, column groups per wave, ring rows), forced, on
+    small-integer data (exact in any summation order) and on normal data
+    against the bar."""
+    m, k, n, N, M, V = shape
+    rt, bv, cpw, rb = variant
+    for key, val in (("PS", 1), ("PSRT", rt), ("PSBV", bv), ("PSCPW", cpw), ("PSRB", rb),
+                     ("SPLITS", splits)):
+        monkeypatch.setenv("NMSPMM_" + key, str(val))
+    name = nm.nmspmm_kernel_name(m, n, k, N, M, V)
+    want = "nm_stream_kernel<r%d,c%d,bv%d,rb%d>" % (16 * rt, 128 * bv * cpw, bv, rb)
+    if not name.startswith(want):
+        pytest.skip(f"variant not available for {shape} ({name})")
+    C, C_ref, _ = parity(m, k, n, N, M, V, "int", seed=31 + m + n)
+    assert bool(np.array_equal(C.astype(np.float64), C_ref)), \
+        f"{name}: {int(np.count_nonzero(C.astype(np.float64) != C_ref))} outputs differ"
+    C, C_ref, Bnd = parity(m, k, n, N, M, V, "normal", seed=37 + m + n)
+    r = oracle.check(C, C_ref, Bnd)
+    assert r, (name, r)
+
+
+def test_stream_kernel_chosen_by_rule(monkeypatch):
+    """The dispatcher takes the pipelined kernel for the sparse levels (ring of
+    16 or 32 rows) above 16 rows: 32-row tiles with split-k for short
+    products, the largest tile that fills the chip for taller ones; and keeps
+    the register-operand kernel for 16-row decode shapes and denser levels."""
+    monkeypatch.delenv("NMSPMM_PS", raising=False)
+    assert nm.nmspmm_kernel_name(64, 8192, 8192, 4, 32, 64) == "nm_stream_kernel<r32,c256,bv2,rb16>+zero,split4"
+    assert nm.nmspmm_kernel_name(1024, 2048, 2048, 4, 32, 32) == "nm_stream_kernel<r32,c256,bv2,rb16>,split1"
+    assert nm.nmspmm_kernel_name(512, 2048, 2048, 8, 32, 32) == "nm_stream_kernel<r16,c256,bv2,rb32>,split1"
+    assert nm.nmspmm_kernel_name(512, 512, 512, 4, 32, 32) == "nm_stream_kernel<r16,c128,bv1,rb16>,split1"
+    assert nm.nmspmm_kernel_name(16, 8192, 8192, 4, 32, 64).startswith("nm_skinny_kernel")
+    assert nm.nmspmm_kernel_name(512, 1024, 1024, 16, 32, 32).startswith("nm_skinny_kernel")
+    monkeypatch.setenv("NMSPMM_PS", "0")
+    assert nm.nmspmm_kernel_name(64, 8192, 8192, 4, 32, 64).startswith("nm_skinny_kernel")
 
 
 def test_dense_comparator_is_true_fp32():
@@ -364,6 +427,8 @@ def test_dense_comparator_is_true_fp32():
 # streaming, streaming split-k, general kernel
 EPI_SHAPES = [
     (2048, 128, 8192, 8, 32, 32),
+    (64, 2048, 2048, 4, 32, 64),     # pipelined streaming kernel, split-k
+    (512, 512, 512, 4, 32, 32),      # pipelined streaming kernel, fused epilogue
     (300, 256, 1088, 8, 32, 32),
     (16, 2048, 640, 4, 32, 128),
     (16, 512, 4096, 4, 32, 64),
