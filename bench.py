@@ -19,6 +19,7 @@ dense fp32 torch.matmul comparison.
 from __future__ import annotations
 
 import argparse
+import ctypes
 import hashlib
 import json
 import os
@@ -65,6 +66,8 @@ def kernel_source_sha(kernel_name):
         files.append(f"nmspmm_tiled_{kernel_name.split('<')[1].split(',')[0]}.hip")
     elif kernel_name.startswith("nm_skinny_kernel<"):
         files.append("nmspmm_skinny.hip")
+    elif kernel_name.startswith("nm_stream_kernel<"):
+        files.append("nmspmm_stream.hip")
     else:
         files.append("nmspmm_kernels.hip")
     h = hashlib.sha256()
@@ -97,6 +100,10 @@ class Workload:
                               tidx if c == 0 else tidx.clone(),
                               torch.empty((run.m, run.n), dtype=torch.float32, device=dev)))
         self.ptrs = [(a.data_ptr(), b.data_ptr(), i.data_ptr(), c.data_ptr()) for a, b, i, c in self.sets]
+        # split-k through a workspace where the kernel takes one (launches on
+        # one stream run one at a time, so one workspace serves every copy)
+        need = nm.nmspmm_workspace_bytes(run.m, run.n, run.k, run.N, run.M, run.V)
+        self.ws = torch.empty(need, dtype=torch.uint8, device=dev) if need > 0 else None
         self.dense = None
         if with_dense:
             tB = torch.from_numpy(Bp).to(dev)
@@ -107,9 +114,20 @@ class Workload:
     def launch(self, i, stream_handle):
         r = self.run
         a, b, x, c = self.ptrs[i % self.copies]
-        st = self.nm.nmspmm_run_ptr(a, b, x, c, r.m, r.n, r.k, r.N, r.M, r.V, stream_handle)
+        if self.ws is None:
+            st = self.nm.nmspmm_run_ptr(a, b, x, c, r.m, r.n, r.k, r.N, r.M, r.V, stream_handle)
+        else:
+            st = self.nm.lib().nmspmm_run_ws(a, b, x, c, r.m, r.n, r.k, r.N, r.M, r.V, ctypes.c_float(1.0),
+                                             None, 0, self.ws.data_ptr(), self.ws.numel(), stream_handle)
         if st != 0:
             raise RuntimeError(f"nmspmm_run failed: {self.nm.nmspmm_status_string(st)}")
+
+    def kernel_label(self):
+        """The kernel variant's name, with "+ws" for the split-k workspace
+        reduction in place of the zero fill and atomics."""
+        r = self.run
+        name = self.nm.nmspmm_kernel_name(r.m, r.n, r.k, r.N, r.M, r.V)
+        return name.replace("+zero,", "+ws,") if self.ws is not None else name
 
     def launch_dense(self, i):
         a, b, c = self.dense[i % self.copies]
@@ -118,6 +136,7 @@ class Workload:
     def free(self):
         self.sets = None
         self.dense = None
+        self.ws = None
 
 
 def warm_gpu(torch, fn, seconds):
@@ -233,7 +252,7 @@ def measure(torch, nm, run, steps, warmup, with_dense, graph=False, warm_seconds
     total_ms, per = time_launches(torch, lambda i: w.launch(i, handle), steps, warmup, warm_seconds)
     res = {
         "workload": run.name, "m": run.m, "n": run.n, "k": run.k, "N": run.N, "M": run.M,
-        "V": run.V, "kernel": nm.nmspmm_kernel_name(run.m, run.n, run.k, run.N, run.M, run.V),
+        "V": run.V, "kernel": w.kernel_label(),
         "copies": w.copies, "ms_per_step": total_ms / steps,
         "kernel_ms_mean": statistics.fmean(per), "timing": "per-launch events",
     }

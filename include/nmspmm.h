@@ -120,6 +120,35 @@ NMSPMM_API nmspmm_status_t nmspmm_run_ex(const float *A, const float *Bc, const 
                               int M, int V, float alpha, const float *bias,
                               nmspmm_act_t act, hipStream_t stream);
 
+/* Bytes of workspace that nmspmm_run_ws can use for a product of this shape,
+ * with buffers aligned as the allocator returns them: 0 when the kernel
+ * chosen for the shape does not split k through a workspace (only the
+ * pipelined streaming kernel for short products at the sparse levels does),
+ * -1 for a bad shape.  Host only, no GPU call. */
+NMSPMM_API int64_t nmspmm_workspace_bytes(int64_t m, int64_t n, int64_t k, int N, int M, int V);
+
+/* nmspmm_run_ex with a caller-provided workspace for split-k (the same
+ * product, Eq. 1 as read above, and the same epilogue).
+ *   workspace: DEVICE memory, 256-byte aligned, contents irrelevant, owned
+ *              by the caller.
+ *   workspace_bytes: its size.  When it is at least nmspmm_workspace_bytes
+ *              for the shape, a launch that splits k stores each
+ *              workgroup's partial tile there, and a second kernel sums the
+ *              partial tiles of every output in a fixed order and applies
+ *              the epilogue: no zero fill of C, no atomics, and the result
+ *              does not vary between runs.  Otherwise (NULL, smaller, or a
+ *              kernel that does not take one) the call runs exactly as
+ *              nmspmm_run_ex.
+ * A workspace serves one call at a time: calls that overlap on one workspace
+ * (on different streams) race.  Arguments, asynchrony and errors otherwise
+ * as nmspmm_run_ex, plus NMSPMM_ERR_UNSUPPORTED for a workspace not aligned
+ * to 256 bytes; the library allocates nothing. */
+NMSPMM_API nmspmm_status_t nmspmm_run_ws(const float *A, const float *Bc, const uint8_t *idx,
+                              float *C, int64_t m, int64_t n, int64_t k, int N,
+                              int M, int V, float alpha, const float *bias,
+                              nmspmm_act_t act, void *workspace, size_t workspace_bytes,
+                              hipStream_t stream);
+
 /* nmspmm_compress on the GPU, for pruning on the fly (same selection rule,
  * same output bytes as the host call: for every window and column block the
  * N row-vectors of largest fp64 squared L2 norm, ties to the smaller offset,

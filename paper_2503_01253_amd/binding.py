@@ -26,8 +26,8 @@ ACTS = {"none": NMSPMM_ACT_NONE, "relu": NMSPMM_ACT_RELU, "gelu": NMSPMM_ACT_GEL
 
 EXPORTS = (
     "nmspmm_bc_elems", "nmspmm_idx_bytes", "nmspmm_compress", "nmspmm_compress_device",
-    "nmspmm_run", "nmspmm_run_ex", "nmspmm_validate_idx", "nmspmm_status_string",
-    "nmspmm_kernel_name",
+    "nmspmm_run", "nmspmm_run_ex", "nmspmm_run_ws", "nmspmm_workspace_bytes", "nmspmm_validate_idx",
+    "nmspmm_status_string", "nmspmm_kernel_name",
 )
 
 
@@ -70,6 +70,11 @@ def lib():
     L.nmspmm_run_ex.restype = I
     L.nmspmm_compress_device.argtypes = [P, I64, I64, I, I, I, P, P, P]
     L.nmspmm_compress_device.restype = I
+    L.nmspmm_run_ws.argtypes = [P, P, P, P, I64, I64, I64, I, I, I, ctypes.c_float, P, I, P,
+                                ctypes.c_size_t, P]
+    L.nmspmm_run_ws.restype = I
+    L.nmspmm_workspace_bytes.argtypes = [I64, I64, I64, I, I, I]
+    L.nmspmm_workspace_bytes.restype = I64
     _lib = L
     return L
 
@@ -145,9 +150,23 @@ def nmspmm_run(A, Bc, idx, C, m: int, n: int, k: int, N: int, M: int, V: int, st
     return nmspmm_run_ex(A, Bc, idx, C, m, n, k, N, M, V, stream=stream, _name="nmspmm_run")
 
 
+def nmspmm_workspace_bytes(m: int, n: int, k: int, N: int, M: int, V: int) -> int:
+    """Workspace bytes nmspmm_run_ws can use for this shape (0: none; -1: bad shape)."""
+    return int(lib().nmspmm_workspace_bytes(m, n, k, N, M, V))
+
+
+def nmspmm_run_ws(A, Bc, idx, C, m: int, n: int, k: int, N: int, M: int, V: int, workspace,
+                  alpha: float = 1.0, bias=None, act: str = "none", stream=None):
+    """nmspmm_run_ex with a split-k workspace: a uint8 CUDA tensor of at least
+    nmspmm_workspace_bytes bytes, 256-byte aligned (or None, or smaller: the
+    call runs as nmspmm_run_ex)."""
+    return nmspmm_run_ex(A, Bc, idx, C, m, n, k, N, M, V, alpha, bias, act, stream,
+                         _name="nmspmm_run_ws", _workspace=workspace)
+
+
 def nmspmm_run_ex(A, Bc, idx, C, m: int, n: int, k: int, N: int, M: int, V: int,
                   alpha: float = 1.0, bias=None, act: str = "none", stream=None,
-                  _name: str = "nmspmm_run_ex"):
+                  _name: str = "nmspmm_run_ex", _workspace=None):
     """C = act(alpha * (A * B_pruned) + bias) on the GPU (alpha = M/N is Eq. 1's
     factor; bias an n-element fp32 CUDA tensor or None; act "none", "relu" or
     "gelu").  Tensors and stream as for nmspmm_run."""
@@ -159,6 +178,8 @@ def nmspmm_run_ex(A, Bc, idx, C, m: int, n: int, k: int, N: int, M: int, V: int,
              ("idx", idx, torch.uint8, w * q), ("C", C, torch.float32, m * n)]
     if bias is not None:
         specs.append(("bias", bias, torch.float32, n))
+    if _workspace is not None:   # any size: too small means no workspace
+        specs.append(("workspace", _workspace, torch.uint8, _workspace.numel()))
     _check_tensors(torch, C, specs)
     if act not in ACTS:
         raise ValueError(f"act must be one of {sorted(ACTS)}")
@@ -168,6 +189,12 @@ def nmspmm_run_ex(A, Bc, idx, C, m: int, n: int, k: int, N: int, M: int, V: int,
         if _name == "nmspmm_run":
             st = L.nmspmm_run(A.data_ptr(), Bc.data_ptr(), idx.data_ptr(), C.data_ptr(),
                               m, n, k, N, M, V, stream.cuda_stream)
+        elif _name == "nmspmm_run_ws":
+            st = L.nmspmm_run_ws(A.data_ptr(), Bc.data_ptr(), idx.data_ptr(), C.data_ptr(),
+                                 m, n, k, N, M, V, float(alpha),
+                                 None if bias is None else bias.data_ptr(), ACTS[act],
+                                 None if _workspace is None else _workspace.data_ptr(),
+                                 0 if _workspace is None else _workspace.numel(), stream.cuda_stream)
         else:
             st = L.nmspmm_run_ex(A.data_ptr(), Bc.data_ptr(), idx.data_ptr(), C.data_ptr(),
                                  m, n, k, N, M, V, float(alpha),

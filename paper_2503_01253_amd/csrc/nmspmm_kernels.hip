@@ -87,6 +87,28 @@ __global__ __launch_bounds__(256) void nm_zero4_kernel(float *__restrict__ C, in
     if (first < count - 4 * count4) C[4 * count4 + first] = 0.f;
 }
 
+// The second half of a split-k launch through a workspace: one thread per
+// output, the partial tiles of its output tile (tile-major, splits
+// consecutive, row-major ROWS x COLS each) summed in split order, then the
+// epilogue.  Consecutive threads take consecutive columns of a tile row.
+__global__ __launch_bounds__(256) void nm_splitk_reduce_kernel(const float *__restrict__ ws,
+                                                               float *__restrict__ C, int64_t m, int64_t n,
+                                                               int rows, int cols, int tiles_n, int splits,
+                                                               Epilogue epi)
+{
+    const int64_t count = m * n;
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < count; i += (int64_t)gridDim.x * 256) {
+        const int64_t row = i / n, col = i - row * n;
+        const int64_t tile = (row / rows) * tiles_n + col / cols;
+        const int64_t e = (row % rows) * cols + col % cols;
+        const int64_t tsz = (int64_t)rows * cols;
+        const float *p = ws + tile * splits * tsz + e;
+        float sum = p[0];
+        for (int s = 1; s < splits; ++s) sum += p[s * tsz];
+        C[i] = apply_epilogue(epi, sum, col);
+    }
+}
+
 // ---------------------------------------------------------------------------
 // Dispatch
 // ---------------------------------------------------------------------------
@@ -135,6 +157,19 @@ struct Plan {
 };
 
 bool aligned(const void *p, int bytes) { return (reinterpret_cast<uintptr_t>(p) % bytes) == 0; }
+
+// Workspace of a split-k launch of the pipelined streaming kernel (0 when
+// the plan does not take one): tiles * splits partial tiles.  Measured on
+// MI355X against atomic adds into a zeroed C: 64 x 8192 x 8192 at 4:32
+// 27.6 -> 25.0 us, 128 x 8192 x 8192 40.5 -> 39.0.  The register-operand
+// streaming kernel keeps the atomics: its 16-row tiles add little, and the
+// reduction pass cost more than they did (16 x 8192 x 8192 15.0 -> 15.8 us).
+int64_t plan_ws_bytes(const Plan &p)
+{
+    if (p.splits <= 1 || p.kind != Kind::Stream) return 0;
+    const int64_t tiles = (int64_t)p.tiles_m * p.tiles_n;
+    return tiles * p.splits * stream_rows(p.RT) * p.COLS * 4;
+}
 
 // Quads per stage actually instantiated for a stage depth of KA columns of A
 // (the smallest that holds RS compressed rows), 0 if none.
@@ -500,13 +535,16 @@ hipError_t launch_general(const float *A, const float *Bc, const uint8_t *idx, f
 
 bool trivial(const Epilogue &e) { return e.alpha == 1.f && !e.bias && e.act == NMSPMM_ACT_NONE; }
 
+// `ws` (plan_ws_bytes(p) bytes) or null: split-k through atomic adds into a
+// zeroed C.
 hipError_t launch_main(const Plan &p, const float *A, const float *Bc, const uint8_t *idx, float *C,
                        int64_t m, int64_t n, int64_t k, int N, int M, int V, const Epilogue &epi,
-                       hipStream_t stream)
+                       void *ws, hipStream_t stream)
 {
     if (p.kind == Kind::General)
         return launch_general(A, Bc, idx, C, m, n, k, N, M, V, epi, stream);
-    if (p.splits > 1) {
+    float *ws_part = static_cast<float *>(ws);
+    if (p.splits > 1 && !ws) {
         const int64_t count = m * n;
         if (aligned(C, 16)) {
             const int64_t blocks = std::min<int64_t>((count / 4 + 255) / 256 + 1, 4096);
@@ -554,6 +592,7 @@ hipError_t launch_main(const Plan &p, const float *A, const float *Bc, const uin
         s.tiles_n = p.tiles_n;
         s.sw = p.SW;
         s.epi = epi;
+        s.ws = ws_part;
         return launch_stream(p.RT, p.BV, p.CPW, p.RB, s, stream);
     }
     TiledArgs a;
@@ -580,9 +619,16 @@ hipError_t launch_main(const Plan &p, const float *A, const float *Bc, const uin
 // epilogue does something, one pass over C that applies it.
 hipError_t launch_plan(const Plan &p, const float *A, const float *Bc, const uint8_t *idx, float *C,
                        int64_t m, int64_t n, int64_t k, int N, int M, int V, const Epilogue &epi,
-                       hipStream_t stream)
+                       void *ws, hipStream_t stream)
 {
-    hipError_t e = launch_main(p, A, Bc, idx, C, m, n, k, N, M, V, epi, stream);
+    hipError_t e = launch_main(p, A, Bc, idx, C, m, n, k, N, M, V, epi, ws, stream);
+    if (e == hipSuccess && ws) {
+        const int rows = stream_rows(p.RT);
+        const int64_t blocks = std::min<int64_t>((m * n + 255) / 256, 8192);
+        hipLaunchKernelGGL(nm_splitk_reduce_kernel, dim3((unsigned)blocks), dim3(256), 0, stream,
+                           static_cast<const float *>(ws), C, m, n, rows, p.COLS, p.tiles_n, p.splits, epi);
+        return hipGetLastError();
+    }
     if (e != hipSuccess || p.kind == Kind::General || p.splits == 1 || trivial(epi)) return e;
     const int64_t count = m * n;
     const int64_t blocks = std::min<int64_t>((count + 255) / 256, 4096);
@@ -627,10 +673,12 @@ extern "C" const char *nmspmm_kernel_name(int64_t m, int64_t n, int64_t k, int N
     return buf;
 }
 
-extern "C" nmspmm_status_t nmspmm_run_ex(const float *A, const float *Bc, const uint8_t *idx,
-                                         float *C, int64_t m, int64_t n, int64_t k, int N, int M,
-                                         int V, float alpha, const float *bias, nmspmm_act_t act,
-                                         hipStream_t stream)
+namespace nmspmm {
+namespace {
+
+nmspmm_status_t run_impl(const float *A, const float *Bc, const uint8_t *idx, float *C, int64_t m, int64_t n,
+                         int64_t k, int N, int M, int V, float alpha, const float *bias, nmspmm_act_t act,
+                         void *workspace, size_t ws_bytes, hipStream_t stream)
 {
     if (!shape_ok(m, n, k, N, M, V)) return NMSPMM_ERR_INVALID_ARG;
     if (act != NMSPMM_ACT_NONE && act != NMSPMM_ACT_RELU && act != NMSPMM_ACT_GELU)
@@ -641,14 +689,47 @@ extern "C" nmspmm_status_t nmspmm_run_ex(const float *A, const float *Bc, const 
     if (k > 0 && (!A || !Bc || !idx)) return NMSPMM_ERR_INVALID_ARG;
     if (!aligned(C, 4) || (k > 0 && (!aligned(A, 4) || !aligned(Bc, 4))) || !aligned(bias, 4))
         return NMSPMM_ERR_UNSUPPORTED;
+    if (workspace && !aligned(workspace, 256)) return NMSPMM_ERR_UNSUPPORTED;
     const Plan p = make_plan(A, Bc, C, m, n, k, N, M, V);
     if (p.kind == Kind::None) return NMSPMM_OK;
     Epilogue epi;
     epi.alpha = alpha;
     epi.bias = bias;
     epi.act = act;
-    const hipError_t e = launch_plan(p, A, Bc, idx, C, m, n, k, N, M, V, epi, stream);
+    // the workspace serves split-k launches of the streaming kernels that it
+    // is large enough for; everything else runs as without one
+    const int64_t need = plan_ws_bytes(p);
+    void *ws = need > 0 && workspace && (uint64_t)need <= (uint64_t)ws_bytes ? workspace : nullptr;
+    const hipError_t e = launch_plan(p, A, Bc, idx, C, m, n, k, N, M, V, epi, ws, stream);
     return e == hipSuccess ? NMSPMM_OK : NMSPMM_ERR_HIP;
+}
+
+}  // namespace
+}  // namespace nmspmm
+
+extern "C" nmspmm_status_t nmspmm_run_ex(const float *A, const float *Bc, const uint8_t *idx,
+                                         float *C, int64_t m, int64_t n, int64_t k, int N, int M,
+                                         int V, float alpha, const float *bias, nmspmm_act_t act,
+                                         hipStream_t stream)
+{
+    return run_impl(A, Bc, idx, C, m, n, k, N, M, V, alpha, bias, act, nullptr, 0, stream);
+}
+
+extern "C" nmspmm_status_t nmspmm_run_ws(const float *A, const float *Bc, const uint8_t *idx,
+                                         float *C, int64_t m, int64_t n, int64_t k, int N, int M,
+                                         int V, float alpha, const float *bias, nmspmm_act_t act,
+                                         void *workspace, size_t workspace_bytes, hipStream_t stream)
+{
+    return run_impl(A, Bc, idx, C, m, n, k, N, M, V, alpha, bias, act, workspace, workspace_bytes, stream);
+}
+
+extern "C" int64_t nmspmm_workspace_bytes(int64_t m, int64_t n, int64_t k, int N, int M, int V)
+{
+    if (!shape_ok(m, n, k, N, M, V) || !sizes_fit(m, n, k)) return -1;
+    if (m == 0 || n == 0) return 0;
+    // buffers aligned as the allocator returns them
+    alignas(64) static const float probe[16] = {};
+    return plan_ws_bytes(make_plan(probe, probe, probe, m, n, k, N, M, V));
 }
 
 extern "C" nmspmm_status_t nmspmm_run(const float *A, const float *Bc, const uint8_t *idx,

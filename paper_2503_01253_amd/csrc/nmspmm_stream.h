@@ -21,6 +21,7 @@ struct StreamArgs {
     int tiles_m, tiles_n;
     int sw;              // windows per stage: sw * M <= stream_stage_cols(), sw * N <= RB
     Epilogue epi;        // applied by the stores when splits == 1
+    float *ws;           // split-k workspace (tiles * splits partial tiles), or null: atomics
 };
 
 int stream_rows(int RT);               // rows of C per workgroup

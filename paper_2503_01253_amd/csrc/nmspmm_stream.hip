@@ -358,6 +358,13 @@ __global__ __launch_bounds__(PS_NT) void nm_stream_kernel(StreamArgs p)
         lds_drain();
         ps_barrier();
     }
+    // split-k with a workspace: the staged tile goes to this workgroup's
+    // slice; a second kernel adds the slices into C
+    if (p.ws) {
+        auto part = [&](int e) { return lds[(e / S::COLS) * S::CST + e % S::COLS]; };
+        splitk_store<S::ROWS, S::COLS, PS_NT>(part, p.ws, tile, split, p.splits);
+        return;
+    }
     // split-k: every thread adds consecutive outputs of the staged tile
     // (coalesced atomics)
     for (int e = tid; e < S::ROWS * S::COLS; e += PS_NT) {

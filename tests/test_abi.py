@@ -22,7 +22,7 @@ def declared_symbols():
 
 def test_library_exports_every_declared_symbol():
     names = declared_symbols()
-    assert len(names) == 9
+    assert len(names) == 11
     assert sorted(nm.EXPORTS) == names
     L = nm.lib()
     for name in names:
@@ -87,6 +87,46 @@ def test_validate_idx_rejects_broken_patterns():
     bad[5, 0], bad[4, 0] = idx[4, 0], idx[5, 0]
     assert nm.nmspmm_validate_idx(bad, k, n, N, M, V) == nm.NMSPMM_ERR_INVALID_ARG
     assert nm.nmspmm_validate_idx(idx, k + 1, n, N, M, V) == nm.NMSPMM_ERR_INVALID_ARG
+
+
+def test_workspace_bytes():
+    """Split-k workspace sizes (host only): one partial tile per (tile, split);
+    0 where the chosen kernel does not split k through a workspace; -1 for a
+    bad shape."""
+    # 16 x 8192 x 8192 at 4:32: register-operand streaming kernel, atomics
+    assert nm.nmspmm_workspace_bytes(16, 8192, 8192, 4, 32, 64) == 0
+    # 64 x 8192 x 8192: pipelined streaming kernel, 64 tiles of 32 x 256, split 4
+    assert nm.nmspmm_workspace_bytes(64, 8192, 8192, 4, 32, 64) == 64 * 4 * 32 * 256 * 4
+    assert nm.nmspmm_workspace_bytes(4096, 4096, 4096, 16, 32, 32) == 0    # tiled, no split
+    assert nm.nmspmm_workspace_bytes(512, 2048, 2048, 4, 32, 32) == 0      # no split
+    assert nm.nmspmm_workspace_bytes(0, 64, 64, 4, 32, 32) == 0
+    assert nm.nmspmm_workspace_bytes(10, 64, 65, 4, 32, 32) == -1
+
+
+def test_run_ws_rejects_misaligned_workspace_before_any_launch():
+    L = nm.lib()
+    st = L.nmspmm_run_ws(256, 256, 256, 256, 64, 2048, 2048, 4, 32, 64, ctypes.c_float(1.0), None, 0,
+                         0x104, 1 << 20, None)
+    assert st == nm.NMSPMM_ERR_UNSUPPORTED
+
+
+def test_dispatch_host_path_without_a_gpu():
+    """Every kernel family's host path (plan, argument packing, launch) on a
+    machine without a GPU: the launch fails with NMSPMM_ERR_HIP and nothing
+    crashes.  (Regression: a general-kernel plan once fell through to the
+    tiled launcher.)  Fake device pointers, so this runs only where no GPU is
+    visible."""
+    torch = pytest.importorskip("torch")
+    if torch.cuda.is_available():
+        pytest.skip("launches with fake pointers: CPU-only check")
+    L = nm.lib()
+    shapes = [(17, 24, 10, 3, 8, 2), (300, 320, 320, 16, 32, 32), (129, 128, 96, 4, 32, 16),
+              (1100, 96, 1280, 16, 32, 64), (64, 8192, 8192, 4, 32, 64), (16, 4096, 512, 4, 32, 64)]
+    for m, k, n, N, M, V in shapes:
+        for ws in (None, 1 << 20):
+            st = L.nmspmm_run_ws(4096, 4096, 4096, 8192, m, n, k, N, M, V, ctypes.c_float(1.0), None, 0,
+                                 ws, 1 << 30 if ws else 0, None)
+            assert st == nm.NMSPMM_ERR_HIP, (m, k, n, N, M, V, st)
 
 
 @pytest.mark.parametrize("args,status", [

@@ -29,11 +29,18 @@ def to_dev(x):
     return torch.from_numpy(np.ascontiguousarray(x)).cuda()
 
 
-def gpu_run(A, Bc, idx, m, n, k, N, M, V, stream=None, fill=float("nan")):
-    """Run the library on host arrays; C starts as NaN so unwritten outputs fail."""
+def gpu_run(A, Bc, idx, m, n, k, N, M, V, stream=None, fill=float("nan"), workspace=False):
+    """Run the library on host arrays; C starts as NaN so unwritten outputs
+    fail.  workspace=True: nmspmm_run_ws with a workspace of the size the
+    shape takes (the launch the benchmark times)."""
     dA, dBc, didx = to_dev(A), to_dev(Bc), to_dev(idx)
     dC = torch.full((m, n), fill, dtype=torch.float32, device="cuda")
-    nm.nmspmm_run(dA, dBc, didx, dC, m, n, k, N, M, V, stream=stream)
+    need = nm.nmspmm_workspace_bytes(m, n, k, N, M, V) if workspace else 0
+    if need > 0:
+        ws = torch.full((need,), 0xFF, dtype=torch.uint8, device="cuda")
+        nm.nmspmm_run_ws(dA, dBc, didx, dC, m, n, k, N, M, V, ws, stream=stream)
+    else:
+        nm.nmspmm_run(dA, dBc, didx, dC, m, n, k, N, M, V, stream=stream)
     torch.cuda.synchronize()
     return dC.cpu().numpy()
 
@@ -117,7 +124,7 @@ def test_parity_full_size_sampled_rows(name):
     say(f"[full] {run.describe()} kernel={nm.nmspmm_kernel_name(m, n, k, N, M, V)}")
     A, Bp, _ = make_run(run)
     Bc, idx = nm.nmspmm_compress(Bp, N, M, V)
-    C = gpu_run(A, Bc, idx, m, n, k, N, M, V)
+    C = gpu_run(A, Bc, idx, m, n, k, N, M, V, workspace=True)
     assert np.isfinite(C).all()
     rng = np.random.default_rng(run.seed)
     rows = {0, m - 1, min(m - 1, 127), min(m - 1, 128), min(m - 1, 255), min(m - 1, 256)}
@@ -145,7 +152,7 @@ def test_shape_sparsity_table_sampled_rows(name):
     say(f"[table] {run.describe()} kernel={nm.nmspmm_kernel_name(m, n, k, N, M, V)}")
     A, Bp, _ = make_run(run)
     Bc, idx = nm.nmspmm_compress(Bp, N, M, V)
-    C = gpu_run(A, Bc, idx, m, n, k, N, M, V)
+    C = gpu_run(A, Bc, idx, m, n, k, N, M, V, workspace=True)
     assert np.isfinite(C).all()
     rng = np.random.default_rng(run.seed)
     rows = np.array(sorted({0, m - 1, 127, 128, 255, 256} | set(int(x) for x in rng.integers(0, m, 6))))
@@ -490,6 +497,105 @@ def test_run_ex_trivial_epilogue_is_nmspmm_run():
     C = gpu_run(A, Bc, idx, m, n, k, N, M, V)
     Y = run_ex(A, Bc, idx, m, n, k, N, M, V, 1.0, None, "none")
     assert bool(np.array_equal(C.view(np.uint32), Y.view(np.uint32)))
+
+
+# ---- split-k through a caller-provided workspace (nmspmm_run_ws) ----
+# the pipelined streaming kernel at 16, 32 and 64 rows, ragged tiles, V = 16,
+# and a split that gets no window of k
+WS_CASES = [
+    ((100, 512, 768, 2, 16, 16), {"PS": "1", "PSRT": "1", "SPLITS": "3"}),
+    ((40, 1536, 512, 4, 32, 64), {"PS": "1", "PSRT": "2", "SPLITS": "3"}),
+    ((70, 1536, 832, 4, 32, 64), {"PS": "1", "PSRT": "4", "SPLITS": "5"}),
+    ((20, 160, 256, 4, 32, 64), {"PS": "1", "PSRT": "1", "SPLITS": "4"}),   # 5 windows: split 3 gets none
+]
+
+
+def new_workspace(m, n, k, N, M, V):
+    need = nm.nmspmm_workspace_bytes(m, n, k, N, M, V)
+    assert need > 0
+    ws = torch.full((need,), 0xFF, dtype=torch.uint8, device="cuda")   # contents irrelevant (NaN bytes)
+    assert ws.data_ptr() % 256 == 0
+    return ws
+
+
+def run_ws(A, Bc, idx, m, n, k, N, M, V, ws, alpha=1.0, bias=None, act="none"):
+    dC = torch.full((m, n), float("nan"), dtype=torch.float32, device="cuda")
+    nm.nmspmm_run_ws(to_dev(A), to_dev(Bc), to_dev(idx), dC, m, n, k, N, M, V, ws, alpha=alpha,
+                     bias=None if bias is None else to_dev(bias), act=act)
+    torch.cuda.synchronize()
+    return dC.cpu().numpy()
+
+
+@pytest.mark.parametrize("shape,env", WS_CASES, ids=["rows16_v16", "rows32", "rows64", "rows16_empty_split"])
+def test_run_ws_split_k(shape, env, monkeypatch):
+    """Split-k through the workspace: bit-exact on small integers (twice in a
+    row on one workspace), the epilogue applied once and exactly, normal data
+    within the bar and bit-identical between runs."""
+    for key, val in env.items():
+        monkeypatch.setenv("NMSPMM_" + key, val)
+    m, k, n, N, M, V = shape
+    name = nm.nmspmm_kernel_name(m, n, k, N, M, V)
+    say(f"[workspace] {shape} {name}")
+    assert "+zero,split" in name
+    ws = new_workspace(m, n, k, N, M, V)
+    A, Bp, _ = make_inputs(m, k, n, N, M, V, 5 + m, "int")
+    Bc, idx = oracle.compress(Bp, N, M, V)
+    C_ref = oracle.spmm(A, Bc, idx, m, n, k, N, M, V)
+    for _ in range(2):
+        C = run_ws(A, Bc, idx, m, n, k, N, M, V, ws)
+        assert bool(np.array_equal(C.astype(np.float64), C_ref))
+    bias = np.random.default_rng(n).integers(-50, 50, n).astype(np.float32)
+    Y = run_ws(A, Bc, idx, m, n, k, N, M, V, ws, alpha=4.0, bias=bias, act="relu")
+    assert bool(np.array_equal(Y.astype(np.float64), oracle.epilogue(C_ref, 4.0, bias, "relu")))
+    A, Bp, _ = make_inputs(m, k, n, N, M, V, 9 + m, "normal")
+    Bc, idx = oracle.compress(Bp, N, M, V)
+    C1 = run_ws(A, Bc, idx, m, n, k, N, M, V, ws)
+    C2 = run_ws(A, Bc, idx, m, n, k, N, M, V, ws)
+    assert bool(np.array_equal(C1.view(np.uint32), C2.view(np.uint32)))
+    r = oracle.check(C1, oracle.spmm(A, Bc, idx, m, n, k, N, M, V), oracle.bound(A, Bc, idx, m, n, k, N, M, V))
+    assert r, (name, r)
+
+
+def test_run_ws_small_or_missing_workspace_runs_as_run_ex():
+    """A workspace smaller than needed, or none, leaves the call to the atomic
+    path of nmspmm_run_ex (within the bar)."""
+    m, k, n, N, M, V = 64, 2048, 2048, 4, 32, 64
+    A, Bp, _ = make_inputs(m, k, n, N, M, V, 77, "normal")
+    Bc, idx = oracle.compress(Bp, N, M, V)
+    C_ref = oracle.spmm(A, Bc, idx, m, n, k, N, M, V)
+    Bnd = oracle.bound(A, Bc, idx, m, n, k, N, M, V)
+    small = torch.zeros(256, dtype=torch.uint8, device="cuda")
+    for ws in (small, None):
+        C = run_ws(A, Bc, idx, m, n, k, N, M, V, ws)
+        assert oracle.check(C, C_ref, Bnd)
+    assert int(small.to(torch.int64).sum()) == 0   # untouched
+
+
+def test_run_ws_graph_replay():
+    """nmspmm_run_ws captured in a HIP graph (it records two kernels, no fill of
+    C and no memset): every replay, with eager work between replays, gives
+    the eager result bit for bit."""
+    m, k, n, N, M, V = 64, 2048, 2048, 4, 32, 64
+    assert "+zero,split" in nm.nmspmm_kernel_name(m, n, k, N, M, V)
+    A, Bp, _ = make_inputs(m, k, n, N, M, V, 78, "normal")
+    Bc, idx = oracle.compress(Bp, N, M, V)
+    dA, dBc, didx = to_dev(A), to_dev(Bc), to_dev(idx)
+    ws = new_workspace(m, n, k, N, M, V)
+    dC = torch.empty((m, n), dtype=torch.float32, device="cuda")
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        nm.nmspmm_run_ws(dA, dBc, didx, dC, m, n, k, N, M, V, ws)
+    torch.cuda.synchronize()
+    eager = dC.cpu().numpy().copy()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        nm.nmspmm_run_ws(dA, dBc, didx, dC, m, n, k, N, M, V, ws)
+    for i in range(3):
+        dC.fill_(float("nan"))
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert bool(np.array_equal(dC.cpu().numpy().view(np.uint32), eager.view(np.uint32))), f"replay {i}"
 
 
 # ---- device packer (nmspmm_compress_device) ----
