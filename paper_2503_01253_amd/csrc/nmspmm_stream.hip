@@ -120,6 +120,19 @@ __device__ __forceinline__ void lds_drain()
     __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (0 << 8) | (3 << 14));
 }
 
+// Split-k through a caller-provided workspace:
+// workgroup `split` of output tile `tile` stores its partial tile, ROWS x COLS
+// floats given by part(e) for e = row * COLS + col, into its own slice of
+// `ws` with coalesced stores; a second kernel (nm_splitk_reduce_kernel) sums
+// the slices in split order and writes C.  Every thread of the workgroup
+// calls this.
+template <int ROWS, int COLS, int NT, class Part>
+__device__ __forceinline__ void splitk_store(Part part, float *__restrict__ ws, int tile, int split, int splits)
+{
+    float *mine = ws + ((int64_t)tile * splits + split) * (ROWS * COLS);
+    for (int e = threadIdx.x; e < ROWS * COLS; e += NT) mine[e] = part(e);
+}
+
 template <int RT, int BV, int CPW, int RB>
 __global__ __launch_bounds__(PS_NT) void nm_stream_kernel(StreamArgs p)
 {

@@ -146,19 +146,6 @@ __device__ __forceinline__ float apply_epilogue(const Epilogue &e, float v, int6
     return v;
 }
 
-// Split-k through a caller-provided workspace (the streaming kernels):
-// workgroup `split` of output tile `tile` stores its partial tile, ROWS x COLS
-// floats given by part(e) for e = row * COLS + col, into its own slice of
-// `ws` with coalesced stores; a second kernel (nm_splitk_reduce_kernel) sums
-// the slices in split order and writes C.  Every thread of the workgroup
-// calls this.
-template <int ROWS, int COLS, int NT, class Part>
-__device__ __forceinline__ void splitk_store(Part part, float *__restrict__ ws, int tile, int split, int splits)
-{
-    float *mine = ws + ((int64_t)tile * splits + split) * (ROWS * COLS);
-    for (int e = threadIdx.x; e < ROWS * COLS; e += NT) mine[e] = part(e);
-}
-
 struct TiledArgs {
     const float *A;
     const float *Bc;
