@@ -68,6 +68,8 @@ def kernel_source_sha(kernel_name):
         files.append("nmspmm_skinny.hip")
     elif kernel_name.startswith("nm_stream_kernel<"):
         files.append("nmspmm_stream.hip")
+    elif kernel_name.startswith("nm_gather_kernel<"):
+        files.append("nmspmm_gather.hip")
     else:
         files.append("nmspmm_kernels.hip")
     h = hashlib.sha256()
@@ -123,11 +125,12 @@ class Workload:
             raise RuntimeError(f"nmspmm_run failed: {self.nm.nmspmm_status_string(st)}")
 
     def kernel_label(self):
-        """The kernel variant's name, with "+ws" for the split-k workspace
-        reduction in place of the zero fill and atomics."""
+        """The kernel variant's name, as launched: with the workspace when the
+        shape takes one."""
         r = self.run
-        name = self.nm.nmspmm_kernel_name(r.m, r.n, r.k, r.N, r.M, r.V)
-        return name.replace("+zero,", "+ws,") if self.ws is not None else name
+        if self.ws is not None:
+            return self.nm.nmspmm_kernel_name_ws(r.m, r.n, r.k, r.N, r.M, r.V)
+        return self.nm.nmspmm_kernel_name(r.m, r.n, r.k, r.N, r.M, r.V)
 
     def launch_dense(self, i):
         a, b, c = self.dense[i % self.copies]
@@ -385,8 +388,7 @@ def main():
         for i in range(args.launches_only):
             w.launch(i, handle)
         torch.cuda.synchronize()
-        log(f"[bench] {args.launches_only} launches of {run.name} "
-            f"({nm.nmspmm_kernel_name(run.m, run.n, run.k, run.N, run.M, run.V)}) done")
+        log(f"[bench] {args.launches_only} launches of {run.name} ({w.kernel_label()}) done")
         return
     log(f"[bench] headline {run.describe()} steps={args.steps} warmup={args.warmup}")
     head, w = measure(torch, nm, run, args.steps, args.warmup, with_dense=True, graph=run.m <= 256)

@@ -122,22 +122,29 @@ NMSPMM_API nmspmm_status_t nmspmm_run_ex(const float *A, const float *Bc, const 
 
 /* Bytes of workspace that nmspmm_run_ws can use for a product of this shape,
  * with buffers aligned as the allocator returns them: 0 when the kernel
- * chosen for the shape does not split k through a workspace (only the
- * pipelined streaming kernel for short products at the sparse levels does),
- * -1 for a bad shape.  Host only, no GPU call. */
+ * chosen for the shape takes none, -1 for a bad shape.  Two kinds of kernel
+ * take one: the direct-gather kernel for products of at most 128 rows with
+ * V a multiple of 32 (a transposed copy of A, k x R floats with R the
+ * smallest of 16, 32, 64 and 128 that holds m; the gather offsets, 4*w*(n/V)
+ * bytes; and partial strips when it splits k), and the pipelined streaming
+ * kernel when it splits k (its partial tiles).  Host only, no GPU call. */
 NMSPMM_API int64_t nmspmm_workspace_bytes(int64_t m, int64_t n, int64_t k, int N, int M, int V);
 
-/* nmspmm_run_ex with a caller-provided workspace for split-k (the same
- * product, Eq. 1 as read above, and the same epilogue).
+/* nmspmm_run_ex with a caller-provided workspace (the same product, Eq. 1
+ * as read above, and the same epilogue).
  *   workspace: DEVICE memory, 256-byte aligned, contents irrelevant, owned
  *              by the caller.
  *   workspace_bytes: its size.  When it is at least nmspmm_workspace_bytes
- *              for the shape, a launch that splits k stores each
- *              workgroup's partial tile there, and a second kernel sums the
- *              partial tiles of every output in a fixed order and applies
- *              the epilogue: no zero fill of C, no atomics, and the result
+ *              for the shape, the call runs the kernels that use it:
+ *              - short products: a first kernel writes A transposed and the
+ *                gather offsets of D into the workspace, and the
+ *                direct-gather kernel reads them;
+ *              - a launch that splits k stores each workgroup's partial
+ *                tile there, and a last kernel sums the partial tiles of
+ *                every output in a fixed order and applies the epilogue.
+ *              Either way: no zero fill of C, no atomics, and the result
  *              does not vary between runs.  Otherwise (NULL, smaller, or a
- *              kernel that does not take one) the call runs exactly as
+ *              shape whose kernel takes none) the call runs exactly as
  *              nmspmm_run_ex.
  * A workspace serves one call at a time: calls that overlap on one workspace
  * (on different streams) race.  Arguments, asynchrony and errors otherwise
@@ -180,6 +187,11 @@ NMSPMM_API const char *nmspmm_status_string(nmspmm_status_t s);
  * call from the same thread.  For benchmark and profile reports; it launches
  * nothing. */
 NMSPMM_API const char *nmspmm_kernel_name(int64_t m, int64_t n, int64_t k, int N, int M, int V);
+
+/* The same for nmspmm_run_ws with a workspace of nmspmm_workspace_bytes
+ * bytes ("+prep": the transposition kernel runs first; "+ws": partial tiles
+ * go through the workspace). */
+NMSPMM_API const char *nmspmm_kernel_name_ws(int64_t m, int64_t n, int64_t k, int N, int M, int V);
 
 #ifdef __cplusplus
 }

@@ -27,7 +27,7 @@ ACTS = {"none": NMSPMM_ACT_NONE, "relu": NMSPMM_ACT_RELU, "gelu": NMSPMM_ACT_GEL
 EXPORTS = (
     "nmspmm_bc_elems", "nmspmm_idx_bytes", "nmspmm_compress", "nmspmm_compress_device",
     "nmspmm_run", "nmspmm_run_ex", "nmspmm_run_ws", "nmspmm_workspace_bytes", "nmspmm_validate_idx",
-    "nmspmm_status_string", "nmspmm_kernel_name",
+    "nmspmm_status_string", "nmspmm_kernel_name", "nmspmm_kernel_name_ws",
 )
 
 
@@ -66,6 +66,8 @@ def lib():
     L.nmspmm_status_string.restype = ctypes.c_char_p
     L.nmspmm_kernel_name.argtypes = [I64, I64, I64, I, I, I]
     L.nmspmm_kernel_name.restype = ctypes.c_char_p
+    L.nmspmm_kernel_name_ws.argtypes = [I64, I64, I64, I, I, I]
+    L.nmspmm_kernel_name_ws.restype = ctypes.c_char_p
     L.nmspmm_run_ex.argtypes = [P, P, P, P, I64, I64, I64, I, I, I, ctypes.c_float, P, I, P]
     L.nmspmm_run_ex.restype = I
     L.nmspmm_compress_device.argtypes = [P, I64, I64, I, I, I, P, P, P]
@@ -98,6 +100,10 @@ def nmspmm_idx_bytes(k: int, n: int, N: int, M: int, V: int) -> int:
 
 def nmspmm_kernel_name(m: int, n: int, k: int, N: int, M: int, V: int) -> str:
     return lib().nmspmm_kernel_name(m, n, k, N, M, V).decode()
+
+
+def nmspmm_kernel_name_ws(m: int, n: int, k: int, N: int, M: int, V: int) -> str:
+    return lib().nmspmm_kernel_name_ws(m, n, k, N, M, V).decode()
 
 
 def nmspmm_compress(B_dense: np.ndarray, N: int, M: int, V: int):

@@ -1,7 +1,9 @@
 // Device half of the C ABI: the general kernel, the split-k zero fill and
 // the dispatch behind nmspmm_run (the tiled MFMA kernel lives in
 // nmspmm_tiled.h, instantiated per tile shape in nmspmm_tiled_*.hip; the
-// streaming kernel for short products in nmspmm_skinny.hip).
+// streaming kernels for short products in nmspmm_skinny.hip and
+// nmspmm_stream.hip; the direct-gather kernel of the workspace entry point in
+// nmspmm_gather.hip).
 //
 // Notation as in the public header: A m x k, Bc w x n, idx w x q (uint8),
 // C m x n; w = (k/M)*N, q = n/V; compressed row u belongs to window u/N.
@@ -14,6 +16,7 @@
 #include <cstring>
 
 #include "nmspmm.h"
+#include "nmspmm_gather.h"
 #include "nmspmm_internal.h"
 #include "nmspmm_skinny.h"
 #include "nmspmm_stream.h"
@@ -146,7 +149,7 @@ const TileInfo *tile_by_name(const char *name)
     return nullptr;
 }
 
-enum class Kind { None, General, Tiled, Skinny, Stream };
+enum class Kind { None, General, Tiled, Skinny, Stream, Gather };
 
 struct Plan {
     Kind kind = Kind::None;
@@ -154,6 +157,8 @@ struct Plan {
     int BV = 0, KA = 0, NQ = 0, RS = 0, stages = 0, splits = 1, tiles_m = 0, tiles_n = 0;
     int QPW = 0, COLS = 0, CW = 0, RT = 1;   // streaming kernels only
     int CPW = 0, RB = 0, SW = 0;             // pipelined streaming kernel only
+    int CT = 0, NW = 0, D = 0;               // direct-gather kernel only
+    int64_t ws_bytes = 0;
 };
 
 bool aligned(const void *p, int bytes) { return (reinterpret_cast<uintptr_t>(p) % bytes) == 0; }
@@ -166,6 +171,7 @@ bool aligned(const void *p, int bytes) { return (reinterpret_cast<uintptr_t>(p) 
 // reduction pass cost more than they did (16 x 8192 x 8192 15.0 -> 15.8 us).
 int64_t plan_ws_bytes(const Plan &p)
 {
+    if (p.kind == Kind::Gather) return p.ws_bytes;
     if (p.splits <= 1 || p.kind != Kind::Stream) return 0;
     const int64_t tiles = (int64_t)p.tiles_m * p.tiles_n;
     return tiles * p.splits * stream_rows(p.RT) * p.COLS * 4;
@@ -521,6 +527,64 @@ Plan make_plan(const float *A, const float *Bc, const float *C, int64_t m, int64
     return p;
 }
 
+// Direct-gather kernel (workspace entry point only): short products whose
+// column blocks hold whole strips.  k is split across workgroups until the
+// grid has about one workgroup per CU, keeping at least 8 quads per wave.
+// Measured on MI355X at k = n = 8192, 4:32, V = 64 (graph replay, against
+// the streaming kernels through the same workspace): 64 rows 26.3 -> 22.1 us,
+// 128 rows 41.0 -> 33.1; at 16 rows it lost (16.4 against 15.0), and split-k
+// through its partial strips lost everywhere it was tried.
+bool plan_gather(const float *Bc, int64_t m, int64_t n, int64_t k, int N, int M, int V, bool force,
+                 Plan &p)
+{
+    if (k == 0 || m > 128 || !aligned(Bc, 16)) return false;
+    if (!force && (m <= 16 || !prefer_streaming(m, k, N, M))) return false;
+    GatherCfg c;
+    c.RT = m <= 16 ? 1 : m <= 32 ? 2 : m <= 64 ? 4 : 8;
+    static const int defaults[9][3] = {{}, {2, 8, 16}, {2, 8, 12}, {}, {2, 8, 8}, {}, {}, {}, {2, 4, 8}};
+    c.CT = env_int("NMSPMM_GCT", defaults[c.RT][0]);
+    c.NW = env_int("NMSPMM_GNW", defaults[c.RT][1]);
+    c.D = env_int("NMSPMM_GD", defaults[c.RT][2]);
+    if (!gather_has(c) || V % (16 * c.CT) != 0) return false;
+    const int64_t w = (k / M) * N, strips = n / (16 * c.CT);
+    const int64_t nquads = (w + 3) / 4;
+    // At offsets, and Bc offsets up to the quads the register ring loads
+    // ahead of the last one (D <= 16)
+    if (k * gather_rows(c.RT) * 4 >= (int64_t(1) << 31)) return false;
+    if ((4 * nquads + 4 * 2 * 16 + 4) * n * 4 >= (int64_t(1) << 31)) return false;
+    if ((n / V) * w >= (int64_t(1) << 29) || strips > (1 << 24)) return false;
+    int64_t splits = 1;
+    if (strips < 256)
+        splits = std::max<int64_t>(1, std::min<int64_t>((256 + strips - 1) / strips, nquads / (8 * c.NW)));
+    const int fs = env_int("NMSPMM_SPLITS", 0);
+    if (fs >= 1) splits = std::min<int64_t>(fs, std::max<int64_t>(nquads, 1));
+    if (strips * splits > INT32_MAX) return false;
+    p.kind = Kind::Gather;
+    p.RT = c.RT;
+    p.CT = c.CT;
+    p.NW = c.NW;
+    p.D = c.D;
+    p.splits = (int)splits;
+    p.tiles_m = 1;
+    p.tiles_n = (int)strips;
+    p.COLS = 16 * c.CT;
+    p.ws_bytes = gather_layout(c, n, k, N, M, V, (int)splits).total;
+    return true;
+}
+
+// The plan of a call that brings a workspace.  NMSPMM_GATHER (tuning sweeps
+// and tests): 0 never takes the direct-gather kernel, 1 takes it wherever it
+// can run.
+Plan make_ws_plan(const float *A, const float *Bc, const float *C, int64_t m, int64_t n, int64_t k, int N,
+                  int M, int V)
+{
+    Plan p;
+    if (m == 0 || n == 0) return p;
+    const int g = env_int("NMSPMM_GATHER", -1);
+    if (g != 0 && plan_gather(Bc, m, n, k, N, M, V, g == 1, p)) return p;
+    return make_plan(A, Bc, C, m, n, k, N, M, V);
+}
+
 hipError_t launch_general(const float *A, const float *Bc, const uint8_t *idx, float *C,
                           int64_t m, int64_t n, int64_t k, int N, int M, int V, const Epilogue &epi,
                           hipStream_t stream)
@@ -544,6 +608,7 @@ hipError_t launch_main(const Plan &p, const float *A, const float *Bc, const uin
     if (p.kind == Kind::General)
         return launch_general(A, Bc, idx, C, m, n, k, N, M, V, epi, stream);
     float *ws_part = static_cast<float *>(ws);
+    if (p.kind == Kind::Gather && !ws) return hipErrorInvalidValue;
     if (p.splits > 1 && !ws) {
         const int64_t count = m * n;
         if (aligned(C, 16)) {
@@ -574,6 +639,23 @@ hipError_t launch_main(const Plan &p, const float *A, const float *Bc, const uin
         s.cw = p.CW;
         s.epi = epi;
         return launch_skinny(p.RT, p.BV, p.QPW, p.COLS, s, stream);
+    }
+    if (p.kind == Kind::Gather) {
+        GatherArgs g;
+        g.A = A;
+        g.Bc = Bc;
+        g.idx = idx;
+        g.C = C;
+        g.m = m;
+        g.n = n;
+        g.k = k;
+        g.N = N;
+        g.M = M;
+        g.V = V;
+        g.splits = p.splits;
+        g.epi = epi;
+        g.ws = ws;
+        return launch_gather(GatherCfg{p.RT, p.CT, p.NW, p.D}, g, stream);
     }
     if (p.kind == Kind::Stream) {
         StreamArgs s;
@@ -622,13 +704,19 @@ hipError_t launch_plan(const Plan &p, const float *A, const float *Bc, const uin
                        void *ws, hipStream_t stream)
 {
     hipError_t e = launch_main(p, A, Bc, idx, C, m, n, k, N, M, V, epi, ws, stream);
-    if (e == hipSuccess && ws) {
-        const int rows = stream_rows(p.RT);
+    if (e == hipSuccess && ws && p.splits > 1) {
+        const float *part = static_cast<const float *>(ws);
+        int rows = stream_rows(p.RT);
+        if (p.kind == Kind::Gather) {
+            part += gather_layout(GatherCfg{p.RT, p.CT, p.NW, p.D}, n, k, N, M, V, p.splits).part / 4;
+            rows = gather_rows(p.RT);
+        }
         const int64_t blocks = std::min<int64_t>((m * n + 255) / 256, 8192);
-        hipLaunchKernelGGL(nm_splitk_reduce_kernel, dim3((unsigned)blocks), dim3(256), 0, stream,
-                           static_cast<const float *>(ws), C, m, n, rows, p.COLS, p.tiles_n, p.splits, epi);
+        hipLaunchKernelGGL(nm_splitk_reduce_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, part, C, m,
+                           n, rows, p.COLS, p.tiles_n, p.splits, epi);
         return hipGetLastError();
     }
+    if (e == hipSuccess && p.kind == Kind::Gather) return e;
     if (e != hipSuccess || p.kind == Kind::General || p.splits == 1 || trivial(epi)) return e;
     const int64_t count = m * n;
     const int64_t blocks = std::min<int64_t>((count + 255) / 256, 4096);
@@ -642,18 +730,26 @@ hipError_t launch_plan(const Plan &p, const float *A, const float *Bc, const uin
 
 using namespace nmspmm;
 
-extern "C" const char *nmspmm_kernel_name(int64_t m, int64_t n, int64_t k, int N, int M, int V)
+namespace {
+
+const char *plan_name(const Plan &p, bool with_ws)
 {
-    if (!shape_ok(m, n, k, N, M, V) || !sizes_fit(m, n, k)) return "invalid";
-    // assume buffers as aligned as the allocator returns them
-    alignas(64) static const float probe[16] = {};
-    const Plan p = make_plan(probe, probe, probe, m, n, k, N, M, V);
     switch (p.kind) {
     case Kind::None: return "none";
     case Kind::General: return "nm_general_kernel";
-    case Kind::Tiled: case Kind::Skinny: case Kind::Stream: break;
+    case Kind::Tiled: case Kind::Skinny: case Kind::Stream: case Kind::Gather: break;
     }
     thread_local char buf[96];
+    if (p.kind == Kind::Gather) {
+        std::snprintf(buf, sizeof buf, "nm_gather_kernel<r%d,c%d,w%d,d%d>+prep,split%d", gather_rows(p.RT),
+                      p.COLS, p.NW, p.D, p.splits);
+        return buf;
+    }
+    if (p.kind == Kind::Stream && with_ws && p.splits > 1) {
+        std::snprintf(buf, sizeof buf, "nm_stream_kernel<r%d,c%d,bv%d,rb%d>+ws,split%d", 16 * p.RT, p.COLS,
+                      p.BV, p.RB, p.splits);
+        return buf;
+    }
     if (p.kind == Kind::Stream) {
         std::snprintf(buf, sizeof buf, "nm_stream_kernel<r%d,c%d,bv%d,rb%d>%s%d", 16 * p.RT, p.COLS,
                       p.BV, p.RB, p.splits > 1 ? "+zero,split" : ",split", p.splits);
@@ -673,6 +769,23 @@ extern "C" const char *nmspmm_kernel_name(int64_t m, int64_t n, int64_t k, int N
     return buf;
 }
 
+}  // namespace
+
+extern "C" const char *nmspmm_kernel_name(int64_t m, int64_t n, int64_t k, int N, int M, int V)
+{
+    if (!shape_ok(m, n, k, N, M, V) || !sizes_fit(m, n, k)) return "invalid";
+    // assume buffers as aligned as the allocator returns them
+    alignas(64) static const float probe[16] = {};
+    return plan_name(make_plan(probe, probe, probe, m, n, k, N, M, V), false);
+}
+
+extern "C" const char *nmspmm_kernel_name_ws(int64_t m, int64_t n, int64_t k, int N, int M, int V)
+{
+    if (!shape_ok(m, n, k, N, M, V) || !sizes_fit(m, n, k)) return "invalid";
+    alignas(64) static const float probe[16] = {};
+    return plan_name(make_ws_plan(probe, probe, probe, m, n, k, N, M, V), true);
+}
+
 namespace nmspmm {
 namespace {
 
@@ -690,14 +803,15 @@ nmspmm_status_t run_impl(const float *A, const float *Bc, const uint8_t *idx, fl
     if (!aligned(C, 4) || (k > 0 && (!aligned(A, 4) || !aligned(Bc, 4))) || !aligned(bias, 4))
         return NMSPMM_ERR_UNSUPPORTED;
     if (workspace && !aligned(workspace, 256)) return NMSPMM_ERR_UNSUPPORTED;
-    const Plan p = make_plan(A, Bc, C, m, n, k, N, M, V);
+    // with a workspace large enough for it, the plan of nmspmm_workspace_bytes;
+    // otherwise that of a call without one
+    Plan p = workspace ? make_ws_plan(A, Bc, C, m, n, k, N, M, V) : make_plan(A, Bc, C, m, n, k, N, M, V);
+    if (workspace && (uint64_t)plan_ws_bytes(p) > (uint64_t)ws_bytes) p = make_plan(A, Bc, C, m, n, k, N, M, V);
     if (p.kind == Kind::None) return NMSPMM_OK;
     Epilogue epi;
     epi.alpha = alpha;
     epi.bias = bias;
     epi.act = act;
-    // the workspace serves split-k launches of the streaming kernels that it
-    // is large enough for; everything else runs as without one
     const int64_t need = plan_ws_bytes(p);
     void *ws = need > 0 && workspace && (uint64_t)need <= (uint64_t)ws_bytes ? workspace : nullptr;
     const hipError_t e = launch_plan(p, A, Bc, idx, C, m, n, k, N, M, V, epi, ws, stream);
@@ -729,7 +843,7 @@ extern "C" int64_t nmspmm_workspace_bytes(int64_t m, int64_t n, int64_t k, int N
     if (m == 0 || n == 0) return 0;
     // buffers aligned as the allocator returns them
     alignas(64) static const float probe[16] = {};
-    return plan_ws_bytes(make_plan(probe, probe, probe, m, n, k, N, M, V));
+    return plan_ws_bytes(make_ws_plan(probe, probe, probe, m, n, k, N, M, V));
 }
 
 extern "C" nmspmm_status_t nmspmm_run(const float *A, const float *Bc, const uint8_t *idx,

@@ -22,7 +22,7 @@ def declared_symbols():
 
 def test_library_exports_every_declared_symbol():
     names = declared_symbols()
-    assert len(names) == 11
+    assert len(names) == 12
     assert sorted(nm.EXPORTS) == names
     L = nm.lib()
     for name in names:
@@ -89,18 +89,34 @@ def test_validate_idx_rejects_broken_patterns():
     assert nm.nmspmm_validate_idx(idx, k + 1, n, N, M, V) == nm.NMSPMM_ERR_INVALID_ARG
 
 
-def test_workspace_bytes():
-    """Split-k workspace sizes (host only): one partial tile per (tile, split);
-    0 where the chosen kernel does not split k through a workspace; -1 for a
-    bad shape."""
-    # 16 x 8192 x 8192 at 4:32: register-operand streaming kernel, atomics
+def test_workspace_bytes(monkeypatch):
+    """Workspace sizes (host only); -1 for a bad shape.  Short products with V
+    a multiple of 32 take the direct-gather kernel: a transposed copy of A
+    (k x 16, 32, 64 or 128 floats), the offsets (4 * w * n/V bytes) and, when
+    k is split, one partial strip of 32 columns per (strip, split).  Without
+    it: one partial tile per (tile, split) of the pipelined streaming kernel,
+    0 where the chosen kernel does not split k through a workspace."""
+    MiB = 1 << 20
+    assert nm.nmspmm_workspace_bytes(64, 8192, 8192, 4, 32, 64) == 2 * MiB + MiB // 2
+    assert nm.nmspmm_workspace_bytes(128, 8192, 8192, 4, 32, 64) == 4 * MiB + MiB // 2
+    # 32 strips of 32 columns, w = 2048: k split 8 ways (8 quads for each of 8 waves)
+    assert nm.nmspmm_workspace_bytes(20, 1024, 16384, 4, 32, 64) == 2 * MiB + 16 * 2048 * 4 + 32 * 8 * 32 * 32 * 4
+    assert nm.nmspmm_kernel_name_ws(20, 1024, 16384, 4, 32, 64) == "nm_gather_kernel<r32,c32,w8,d12>+prep,split8"
+    # 16 rows keep the register-operand streaming kernel (atomics, no workspace)
     assert nm.nmspmm_workspace_bytes(16, 8192, 8192, 4, 32, 64) == 0
-    # 64 x 8192 x 8192: pipelined streaming kernel, 64 tiles of 32 x 256, split 4
-    assert nm.nmspmm_workspace_bytes(64, 8192, 8192, 4, 32, 64) == 64 * 4 * 32 * 256 * 4
+    monkeypatch.setenv("NMSPMM_GATHER", "1")
+    assert nm.nmspmm_workspace_bytes(16, 8192, 8192, 4, 32, 64) == MiB // 2 + MiB // 2
+    monkeypatch.delenv("NMSPMM_GATHER")
     assert nm.nmspmm_workspace_bytes(4096, 4096, 4096, 16, 32, 32) == 0    # tiled, no split
     assert nm.nmspmm_workspace_bytes(512, 2048, 2048, 4, 32, 32) == 0      # no split
     assert nm.nmspmm_workspace_bytes(0, 64, 64, 4, 32, 32) == 0
     assert nm.nmspmm_workspace_bytes(10, 64, 65, 4, 32, 32) == -1
+    monkeypatch.setenv("NMSPMM_GATHER", "0")
+    # 16 x 8192 x 8192 at 4:32: register-operand streaming kernel, atomics
+    assert nm.nmspmm_workspace_bytes(16, 8192, 8192, 4, 32, 64) == 0
+    # 64 x 8192 x 8192: pipelined streaming kernel, 64 tiles of 32 x 256, split 4
+    assert nm.nmspmm_workspace_bytes(64, 8192, 8192, 4, 32, 64) == 64 * 4 * 32 * 256 * 4
+    assert nm.nmspmm_kernel_name_ws(64, 8192, 8192, 4, 32, 64) == "nm_stream_kernel<r32,c256,bv2,rb16>+ws,split4"
 
 
 def test_run_ws_rejects_misaligned_workspace_before_any_launch():
@@ -121,7 +137,8 @@ def test_dispatch_host_path_without_a_gpu():
         pytest.skip("launches with fake pointers: CPU-only check")
     L = nm.lib()
     shapes = [(17, 24, 10, 3, 8, 2), (300, 320, 320, 16, 32, 32), (129, 128, 96, 4, 32, 16),
-              (1100, 96, 1280, 16, 32, 64), (64, 8192, 8192, 4, 32, 64), (16, 4096, 512, 4, 32, 64)]
+              (1100, 96, 1280, 16, 32, 64), (64, 8192, 8192, 4, 32, 64), (16, 4096, 512, 4, 32, 64),
+              (20, 16384, 1024, 4, 32, 64)]
     for m, k, n, N, M, V in shapes:
         for ws in (None, 1 << 20):
             st = L.nmspmm_run_ws(4096, 4096, 4096, 8192, m, n, k, N, M, V, ctypes.c_float(1.0), None, 0,

@@ -121,7 +121,7 @@ def test_parity_full_size_sampled_rows(name):
     the oracle computes a sample of rows (first, last, tile edges, random)."""
     run = RUNS[name]
     m, k, n, N, M, V = run.m, run.k, run.n, run.N, run.M, run.V
-    say(f"[full] {run.describe()} kernel={nm.nmspmm_kernel_name(m, n, k, N, M, V)}")
+    say(f"[full] {run.describe()} kernel={nm.nmspmm_kernel_name_ws(m, n, k, N, M, V)}")
     A, Bp, _ = make_run(run)
     Bc, idx = nm.nmspmm_compress(Bp, N, M, V)
     C = gpu_run(A, Bc, idx, m, n, k, N, M, V, workspace=True)
@@ -149,7 +149,7 @@ def test_shape_sparsity_table_sampled_rows(name):
     the benchmark times; the oracle computes a sample of rows."""
     run = TABLE[name]
     m, k, n, N, M, V = run.m, run.k, run.n, run.N, run.M, run.V
-    say(f"[table] {run.describe()} kernel={nm.nmspmm_kernel_name(m, n, k, N, M, V)}")
+    say(f"[table] {run.describe()} kernel={nm.nmspmm_kernel_name_ws(m, n, k, N, M, V)}")
     A, Bp, _ = make_run(run)
     Bc, idx = nm.nmspmm_compress(Bp, N, M, V)
     C = gpu_run(A, Bc, idx, m, n, k, N, M, V, workspace=True)
@@ -533,10 +533,11 @@ def test_run_ws_split_k(shape, env, monkeypatch):
     within the bar and bit-identical between runs."""
     for key, val in env.items():
         monkeypatch.setenv("NMSPMM_" + key, val)
+    monkeypatch.setenv("NMSPMM_GATHER", "0")
     m, k, n, N, M, V = shape
-    name = nm.nmspmm_kernel_name(m, n, k, N, M, V)
+    name = nm.nmspmm_kernel_name_ws(m, n, k, N, M, V)
     say(f"[workspace] {shape} {name}")
-    assert "+zero,split" in name
+    assert "+ws,split" in name
     ws = new_workspace(m, n, k, N, M, V)
     A, Bp, _ = make_inputs(m, k, n, N, M, V, 5 + m, "int")
     Bc, idx = oracle.compress(Bp, N, M, V)
@@ -571,12 +572,17 @@ def test_run_ws_small_or_missing_workspace_runs_as_run_ex():
     assert int(small.to(torch.int64).sum()) == 0   # untouched
 
 
-def test_run_ws_graph_replay():
-    """nmspmm_run_ws captured in a HIP graph (it records two kernels, no fill of
-    C and no memset): every replay, with eager work between replays, gives
-    the eager result bit for bit."""
+@pytest.mark.parametrize("gather", ["0", "1"])
+def test_run_ws_graph_replay(gather, monkeypatch):
+    """nmspmm_run_ws captured in a HIP graph (two kernels, no fill of C and no
+    memset: split-k of the pipelined streaming kernel, or the transposition
+    pass and the direct-gather kernel): every replay, with eager work between
+    replays, gives the eager result bit for bit."""
+    monkeypatch.setenv("NMSPMM_GATHER", gather)
     m, k, n, N, M, V = 64, 2048, 2048, 4, 32, 64
-    assert "+zero,split" in nm.nmspmm_kernel_name(m, n, k, N, M, V)
+    name = nm.nmspmm_kernel_name_ws(m, n, k, N, M, V)
+    say(f"[graph] {name}")
+    assert ("+ws,split" if gather == "0" else "nm_gather_kernel") in name
     A, Bp, _ = make_inputs(m, k, n, N, M, V, 78, "normal")
     Bc, idx = oracle.compress(Bp, N, M, V)
     dA, dBc, didx = to_dev(A), to_dev(Bc), to_dev(idx)
@@ -596,6 +602,82 @@ def test_run_ws_graph_replay():
         g.replay()
         torch.cuda.synchronize()
         assert bool(np.array_equal(dC.cpu().numpy().view(np.uint32), eager.view(np.uint32))), f"replay {i}"
+
+
+# ---- direct-gather kernel (nmspmm_run_ws on short products) ----
+GATHER_SHAPES = [
+    (1, 512, 256, 4, 32, 32),       # one row
+    (5, 1024, 512, 2, 4, 32),
+    (16, 2048, 1024, 4, 32, 64),
+    (17, 776, 320, 3, 8, 32),       # w = 291: ragged last quad
+    (40, 1536, 512, 4, 32, 64),
+    (64, 1000, 512, 5, 8, 64),      # w = 625
+    (100, 832, 768, 1, 8, 128),     # w = 104, four strips per column block
+    (128, 2048, 1024, 16, 32, 32),  # 50 %
+    (128, 96, 64, 8, 32, 32),       # w = 24: one to two quads per wave
+    (33, 32, 256, 4, 32, 32),       # one window: most waves get no quad
+    (70, 2040, 96, 3, 8, 32),       # w = 765, three strips
+]
+
+
+@pytest.mark.parametrize("splits", ["auto", "3"])
+@pytest.mark.parametrize("shape", GATHER_SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_gather_kernel_exact(shape, splits, monkeypatch):
+    """The direct-gather kernel (forced), with and without split-k: bit-exact on
+    small integers twice in a row on one workspace, the epilogue applied once
+    and exactly, normal data within the bar and bit-identical between runs."""
+    monkeypatch.setenv("NMSPMM_GATHER", "1")
+    if splits != "auto":
+        monkeypatch.setenv("NMSPMM_SPLITS", splits)
+    m, k, n, N, M, V = shape
+    name = nm.nmspmm_kernel_name_ws(m, n, k, N, M, V)
+    say(f"[gather] {shape} {name}")
+    assert name.startswith("nm_gather_kernel<r%d," % (16 if m <= 16 else 32 if m <= 32 else 64 if m <= 64 else 128))
+    w = k // M * N
+    if splits != "auto" and (w + 3) // 4 >= 3:
+        assert name.endswith(",split3")
+    ws = new_workspace(m, n, k, N, M, V)
+    A, Bp, _ = make_inputs(m, k, n, N, M, V, 11 + m, "int")
+    Bc, idx = oracle.compress(Bp, N, M, V)
+    C_ref = oracle.spmm(A, Bc, idx, m, n, k, N, M, V)
+    for _ in range(2):
+        C = run_ws(A, Bc, idx, m, n, k, N, M, V, ws)
+        assert bool(np.array_equal(C.astype(np.float64), C_ref)), \
+            f"{int(np.count_nonzero(C.astype(np.float64) != C_ref))} outputs differ"
+    bias = np.random.default_rng(n).integers(-50, 50, n).astype(np.float32)
+    Y = run_ws(A, Bc, idx, m, n, k, N, M, V, ws, alpha=4.0, bias=bias, act="relu")
+    assert bool(np.array_equal(Y.astype(np.float64), oracle.epilogue(C_ref, 4.0, bias, "relu")))
+    A, Bp, _ = make_inputs(m, k, n, N, M, V, 13 + m, "normal")
+    Bc, idx = oracle.compress(Bp, N, M, V)
+    C1 = run_ws(A, Bc, idx, m, n, k, N, M, V, ws)
+    C2 = run_ws(A, Bc, idx, m, n, k, N, M, V, ws)
+    assert bool(np.array_equal(C1.view(np.uint32), C2.view(np.uint32)))
+    r = oracle.check(C1, oracle.spmm(A, Bc, idx, m, n, k, N, M, V), oracle.bound(A, Bc, idx, m, n, k, N, M, V))
+    assert r, (name, r)
+
+
+def test_gather_kernel_reused_workspace_smaller_shape(monkeypatch):
+    """One workspace, a large call then a smaller one of another row count: the
+    second call's transposed copy and offsets replace the first's."""
+    monkeypatch.setenv("NMSPMM_GATHER", "1")
+    big, small = (128, 2048, 1024, 4, 32, 32), (20, 1024, 512, 4, 32, 64)
+    ws = new_workspace(*[big[i] for i in (0, 2, 1, 3, 4, 5)])
+    assert ws.numel() >= nm.nmspmm_workspace_bytes(*[small[i] for i in (0, 2, 1, 3, 4, 5)])
+    for m, k, n, N, M, V in (big, small):
+        A, Bp, _ = make_inputs(m, k, n, N, M, V, 21 + m, "int")
+        Bc, idx = oracle.compress(Bp, N, M, V)
+        C = run_ws(A, Bc, idx, m, n, k, N, M, V, ws)
+        assert bool(np.array_equal(C.astype(np.float64), oracle.spmm(A, Bc, idx, m, n, k, N, M, V)))
+
+
+def test_gather_kernel_chosen_by_rule():
+    """With a workspace, the 64- and 128-row products of the benchmark take
+    the direct-gather kernel; 16 rows, V = 16 and tall products do not."""
+    assert nm.nmspmm_kernel_name_ws(64, 8192, 8192, 4, 32, 64).startswith("nm_gather_kernel<r64,c32,")
+    assert nm.nmspmm_kernel_name_ws(128, 8192, 8192, 4, 32, 64).startswith("nm_gather_kernel<r128,c32,")
+    assert not nm.nmspmm_kernel_name_ws(16, 8192, 8192, 4, 32, 64).startswith("nm_gather")
+    assert not nm.nmspmm_kernel_name_ws(64, 2048, 2048, 4, 32, 16).startswith("nm_gather")
+    assert not nm.nmspmm_kernel_name_ws(4096, 4096, 4096, 16, 32, 32).startswith("nm_gather")
 
 
 # ---- device packer (nmspmm_compress_device) ----
