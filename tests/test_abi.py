@@ -198,3 +198,17 @@ def test_run_ex_and_compress_device_argument_checks():
     assert L.nmspmm_compress_device(0, 0, 64, 4, 32, 32, 0, 0, None) == nm.NMSPMM_OK
     assert L.nmspmm_compress_device(0, 64, 64, 4, 32, 32, 0, 0, None) == nm.NMSPMM_ERR_INVALID_ARG
     assert L.nmspmm_compress_device(4098, 64, 64, 4, 32, 32, 4096, 4096, None) == nm.NMSPMM_ERR_UNSUPPORTED
+
+
+def test_gather_variant_list_matches_the_source():
+    """The GPU tests force every direct-gather instantiation; their list must
+    be the source's."""
+    src = open(os.path.join(ROOT, "paper_2503_01253_amd", "csrc", "nmspmm_gather.hip")).read()
+    block = src[src.index("#define NM_GATHER_CONFIGS(X)"):]
+    block = block[:block.index("\n\n")]
+    found = [tuple(int(x) for x in t) for t in re.findall(r"X\((\d+), (\d+), (\d+), (\d+)\)", block)]
+    gpu = open(os.path.join(ROOT, "tests", "test_gpu_parity.py")).read()
+    listed = gpu[gpu.index("GATHER_VARIANTS = ["):]
+    listed = listed[:listed.index("]\n")]
+    tested = [tuple(int(x) for x in t) for t in re.findall(r"\((\d+), (\d+), (\d+), (\d+)\)", listed)]
+    assert found and sorted(found) == sorted(tested)

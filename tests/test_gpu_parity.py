@@ -656,6 +656,42 @@ def test_gather_kernel_exact(shape, splits, monkeypatch):
     assert r, (name, r)
 
 
+# every instantiated variant {RT, CT, NW, D}; tests/test_abi.py checks this list against the source
+GATHER_VARIANTS = [
+    (1, 2, 8, 16), (1, 2, 4, 16), (1, 4, 8, 12), (1, 4, 4, 16),
+    (2, 2, 8, 12), (2, 4, 8, 8), (2, 4, 4, 12),
+    (4, 2, 8, 8), (4, 2, 8, 12), (4, 2, 4, 12), (4, 4, 8, 8), (4, 4, 4, 8), (4, 4, 4, 12),
+    (8, 2, 4, 8), (8, 2, 8, 8), (8, 2, 4, 12), (8, 4, 4, 6), (8, 4, 4, 8), (8, 4, 8, 6),
+]
+# per row-tile count: a ragged shape (w not a multiple of 4 where N allows) with V a multiple of 64
+GATHER_VARIANT_SHAPES = {1: (9, 1024, 512, 4, 32, 64), 2: (30, 776, 384, 3, 8, 64),
+                         4: (50, 1000, 512, 5, 8, 64), 8: (100, 832, 768, 1, 8, 128)}
+
+
+@pytest.mark.parametrize("splits", [1, 3])
+@pytest.mark.parametrize("variant", GATHER_VARIANTS, ids=lambda v: "rt%d_ct%d_nw%d_d%d" % v)
+def test_gather_variants_exact(variant, splits, monkeypatch):
+    """Every direct-gather instantiation, forced, with and without split-k:
+    bit-exact on small integers and within the bar on normal data."""
+    rt, ct, nw, d = variant
+    for key, val in (("GATHER", 1), ("GCT", ct), ("GNW", nw), ("GD", d), ("SPLITS", splits)):
+        monkeypatch.setenv("NMSPMM_" + key, str(val))
+    m, k, n, N, M, V = GATHER_VARIANT_SHAPES[rt]
+    name = nm.nmspmm_kernel_name_ws(m, n, k, N, M, V)
+    say(f"[gather variant] {variant} split{splits} {name}")
+    assert name == f"nm_gather_kernel<r{16 * rt},c{16 * ct},w{nw},d{d}>+prep,split{splits}"
+    ws = new_workspace(m, n, k, N, M, V)
+    A, Bp, _ = make_inputs(m, k, n, N, M, V, 31 + m, "int")
+    Bc, idx = oracle.compress(Bp, N, M, V)
+    C = run_ws(A, Bc, idx, m, n, k, N, M, V, ws)
+    assert bool(np.array_equal(C.astype(np.float64), oracle.spmm(A, Bc, idx, m, n, k, N, M, V)))
+    A, Bp, _ = make_inputs(m, k, n, N, M, V, 37 + m, "normal")
+    Bc, idx = oracle.compress(Bp, N, M, V)
+    C = run_ws(A, Bc, idx, m, n, k, N, M, V, ws)
+    r = oracle.check(C, oracle.spmm(A, Bc, idx, m, n, k, N, M, V), oracle.bound(A, Bc, idx, m, n, k, N, M, V))
+    assert r, (name, r)
+
+
 def test_gather_kernel_reused_workspace_smaller_shape(monkeypatch):
     """One workspace, a large call then a smaller one of another row count: the
     second call's transposed copy and offsets replace the first's."""
