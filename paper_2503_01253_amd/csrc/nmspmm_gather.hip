@@ -12,15 +12,16 @@
 // per-block column indices of Sec. III-C.1, laid out u-contiguous per
 // block).  The second pass then gathers At rows straight into registers.
 //
-// Strip kernel: a workgroup owns all rows (16*RT) x 32 columns of C (one
-// strip inside one column block, V a multiple of 32) and, with split-k, a
+// Strip kernel: a workgroup owns all rows (16*RT) x 16*CT columns of C (one
+// strip inside one column block, V a multiple of 16*CT) and, with split-k, a
 // range of quads (4 consecutive compressed rows, the K of
 // v_mfma_f32_16x16x4_f32).  Its NW waves split that range and each streams
 // its quads through a ring of D quads in flight in registers: per quad a
 // lane loads one offset, RT consecutive At floats (rows RT*(l%16)+t, one
-// per row tile t) and two Bc floats (columns 2*(l%16)+s, one per column tile
-// s), and issues 2*RT MFMAs.  No LDS and no barrier in the loop; the waves'
-// partial strips are summed through LDS at the end, in wave order.
+// per row tile t) and CT consecutive Bc floats (columns CT*(l%16)+s, one per
+// column tile s), and issues RT*CT MFMAs.  No LDS and no barrier in the
+// loop; the waves' partial strips are summed through LDS at the end, in a
+// fixed order.
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
