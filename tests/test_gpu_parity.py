@@ -15,7 +15,7 @@ from nm_workloads import RUNS, make_inputs, make_run, table_runs
 torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
 
-if not torch.cuda.is_available():  # the -m gpu suite only runs on a GPU machine
+if not torch.cuda.is_available():  # the -m gpu suite needs a visible GPU
     pytest.skip("no GPU", allow_module_level=True)
 
 import paper_2503_01253_amd as nm  # noqa: E402
