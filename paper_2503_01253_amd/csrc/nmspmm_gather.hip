@@ -17,9 +17,9 @@
 // range of quads (4 consecutive compressed rows, the K of
 // v_mfma_f32_16x16x4_f32).  Its NW waves split that range and each streams
 // its quads through a ring of D quads in flight in registers: per quad a
-// lane loads one offset, RT consecutive At floats (rows RT*(l%16)+t, one
-// per row tile t) and CT consecutive Bc floats (columns CT*(l%16)+s, one per
-// column tile s), and issues RT*CT MFMAs.  No LDS and no barrier in the
+// lane loads one offset, RT At floats (one per row tile t, see c_row) and CT
+// consecutive Bc floats (columns CT*(l%16)+s, one per column tile s), and
+// issues RT*CT MFMAs.  No LDS and no barrier in the
 // loop; the waves' partial strips are summed through LDS at the end, in a
 // fixed order.
 #include <hip/hip_runtime.h>
@@ -95,6 +95,18 @@ __global__ __launch_bounds__(256) void nm_gather_prep_kernel(const float *__rest
     }
 }
 
+// A lane's At floats: RH = min(RT, 4) consecutive rows per 16-byte load, and
+// RT/RH such loads, half h covering rows [16*RH*h, 16*RH*(h+1)) of the At row
+// (so that each load reads one contiguous piece of the row).  MFMA row tile t,
+// MFMA row i then holds row  (t/RH)*16*RH + RH*i + t%RH  of C.
+template <int RT> constexpr int rows_per_load() { return RT < 4 ? RT : 4; }
+template <int RT>
+__device__ __forceinline__ int c_row(int t, int i)
+{
+    constexpr int RH = rows_per_load<RT>();
+    return (t / RH) * 16 * RH + RH * i + t % RH;
+}
+
 template <int RT> struct AOp;
 template <> struct AOp<1> { float v[1]; };
 template <> struct AOp<2> { float v[2]; };
@@ -114,7 +126,7 @@ __device__ __forceinline__ void load_a(AOp<RT> &a, __amdgpu_buffer_rsrc_t rs, ui
 #pragma unroll
         for (int h = 0; h < RT / 4; ++h) {
             const f32x4 x =
-                __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, (int)(voff + 16 * h), 0, 0));
+                __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, (int)(voff + 256 * h), 0, 0));
 #pragma unroll
             for (int i = 0; i < 4; ++i) a.v[4 * h + i] = x[i];
         }
@@ -199,7 +211,7 @@ __global__ __launch_bounds__(NW * 64) void nm_gather_kernel(
     const auto rs_bc = make_rsrc(Bc + u_lo * n + j0, (uint32_t)(max64(u_hi - u_lo, 0) * n * 4));
     const uint32_t lane_off = kq * 4;
     const uint32_t lane_bc = (uint32_t)((kq * n + CT * r) * 4);
-    const uint32_t lane_at = r * RT * 4;
+    const uint32_t lane_at = r * rows_per_load<RT>() * 4;
     const uint32_t quad_bc = (uint32_t)(16 * n);   // bytes of 4 Bc rows
 
     f32x4 acc[RT][CT];
@@ -220,7 +232,7 @@ __global__ __launch_bounds__(NW * 64) void nm_gather_kernel(
     // at the loop head stay exact.
 #pragma unroll
     for (int j = 0; j < D; ++j) {
-        load_a<RT>(av[j], rs_at, OOB + 64 * j);   // distinct offsets: not merged into one load
+        load_a<RT>(av[j], rs_at, OOB + 1024 * j);   // distinct offsets: no two loads merged
         load_b<CT>(bv[j], rs_bc, OOB + 64 * j, 0);
         ov[j] = __builtin_amdgcn_raw_buffer_load_b32(rs_off, (int)lane_off, j * 16, 0);
         __builtin_amdgcn_sched_barrier(0);
@@ -257,7 +269,7 @@ __global__ __launch_bounds__(NW * 64) void nm_gather_kernel(
                 for (int s = 0; s < CT; ++s)
 #pragma unroll
                     for (int i = 0; i < 4; ++i) {
-                        float &x = mine[(RT * (4 * kq + i) + t) * RST + CT * r + s];
+                        float &x = mine[c_row<RT>(t, 4 * kq + i) * RST + CT * r + s];
                         x = round == 0 ? acc[t][s][i] : x + acc[t][s][i];
                     }
         }
