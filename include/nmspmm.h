@@ -123,7 +123,7 @@ NMSPMM_API nmspmm_status_t nmspmm_run_ex(const float *A, const float *Bc, const 
 /* Bytes of workspace that nmspmm_run_ws can use for a product of this shape,
  * with buffers aligned as the allocator returns them: 0 when the kernel
  * chosen for the shape takes none, -1 for a bad shape.  Two kinds of kernel
- * take one: the direct-gather kernel for products of at most 128 rows with
+ * take one: the direct-gather kernel for products of 17 to 128 rows with
  * V a multiple of 32 (a transposed copy of A, k x R floats with R the
  * smallest of 16, 32, 64 and 128 that holds m; the gather offsets, 4*w*(n/V)
  * bytes; and partial strips when it splits k), and the pipelined streaming
