@@ -638,6 +638,8 @@ hipError_t launch_main(const Plan &p, const float *A, const float *Bc, const uin
         s.tiles_n = p.tiles_n;
         s.cw = p.CW;
         s.epi = epi;
+        // Bc streamed past L2: at least 16 MB, four XCDs' worth
+        s.stream_b = (k / M) * N * n * 4 >= (int64_t(16) << 20) ? 1 : 0;
         return launch_skinny(p.RT, p.BV, p.QPW, p.COLS, s, stream);
     }
     if (p.kind == Kind::Gather) {

@@ -21,6 +21,7 @@ struct SkinnyArgs {
     int tiles_m, tiles_n;
     int cw;              // windows per staged chunk of A: cw * M <= skinny_chunk_cols(RT)
     Epilogue epi;        // applied by the stores when splits == 1
+    int stream_b;        // 1: Bc loads with the non-temporal hint (Bc much larger than L2)
 };
 
 int skinny_rows(int RT);        // rows of C per workgroup with RT row tiles
