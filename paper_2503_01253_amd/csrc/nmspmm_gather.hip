@@ -318,10 +318,10 @@ hipError_t launch_cfg(const GatherArgs &a, hipStream_t stream)
 
 // Instantiated configurations: {RT, CT, NW, D}.
 #define NM_GATHER_CONFIGS(X)                                                                            \
-    X(1, 2, 8, 16) X(1, 2, 4, 16) X(1, 4, 8, 12) X(1, 4, 4, 16)                                         \
-    X(2, 2, 8, 12) X(2, 4, 8, 8) X(2, 4, 4, 12)                                                         \
-    X(4, 2, 8, 8) X(4, 2, 8, 12) X(4, 2, 4, 12) X(4, 4, 8, 8) X(4, 4, 4, 8) X(4, 4, 4, 12)              \
-    X(8, 2, 4, 8) X(8, 2, 8, 8) X(8, 2, 4, 12) X(8, 4, 4, 6) X(8, 4, 4, 8) X(8, 4, 8, 6)
+    X(1, 2, 8, 4) X(1, 2, 8, 8) X(1, 4, 8, 4) X(1, 4, 4, 8)                                             \
+    X(2, 2, 8, 4) X(2, 2, 8, 8) X(2, 4, 8, 4)                                                           \
+    X(4, 2, 8, 4) X(4, 2, 8, 3) X(4, 2, 8, 8) X(4, 4, 8, 4) X(4, 4, 4, 8)                               \
+    X(8, 2, 4, 4) X(8, 2, 4, 8) X(8, 2, 8, 4) X(8, 4, 4, 4) X(8, 4, 4, 6)
 
 }  // namespace
 

@@ -101,7 +101,7 @@ def test_workspace_bytes(monkeypatch):
     assert nm.nmspmm_workspace_bytes(128, 8192, 8192, 4, 32, 64) == 4 * MiB + MiB // 2
     # 32 strips of 32 columns, w = 2048: k split 8 ways (8 quads for each of 8 waves)
     assert nm.nmspmm_workspace_bytes(20, 1024, 16384, 4, 32, 64) == 2 * MiB + 16 * 2048 * 4 + 32 * 8 * 32 * 32 * 4
-    assert nm.nmspmm_kernel_name_ws(20, 1024, 16384, 4, 32, 64) == "nm_gather_kernel<r32,c32,w8,d12>+prep,split8"
+    assert nm.nmspmm_kernel_name_ws(20, 1024, 16384, 4, 32, 64) == "nm_gather_kernel<r32,c32,w8,d4>+prep,split8"
     # 16 rows keep the register-operand streaming kernel (atomics, no workspace)
     assert nm.nmspmm_workspace_bytes(16, 8192, 8192, 4, 32, 64) == 0
     monkeypatch.setenv("NMSPMM_GATHER", "1")

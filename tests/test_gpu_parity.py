@@ -658,10 +658,10 @@ def test_gather_kernel_exact(shape, splits, monkeypatch):
 
 # every instantiated variant {RT, CT, NW, D}; tests/test_abi.py checks this list against the source
 GATHER_VARIANTS = [
-    (1, 2, 8, 16), (1, 2, 4, 16), (1, 4, 8, 12), (1, 4, 4, 16),
-    (2, 2, 8, 12), (2, 4, 8, 8), (2, 4, 4, 12),
-    (4, 2, 8, 8), (4, 2, 8, 12), (4, 2, 4, 12), (4, 4, 8, 8), (4, 4, 4, 8), (4, 4, 4, 12),
-    (8, 2, 4, 8), (8, 2, 8, 8), (8, 2, 4, 12), (8, 4, 4, 6), (8, 4, 4, 8), (8, 4, 8, 6),
+    (1, 2, 8, 4), (1, 2, 8, 8), (1, 4, 8, 4), (1, 4, 4, 8),
+    (2, 2, 8, 4), (2, 2, 8, 8), (2, 4, 8, 4),
+    (4, 2, 8, 4), (4, 2, 8, 3), (4, 2, 8, 8), (4, 4, 8, 4), (4, 4, 4, 8),
+    (8, 2, 4, 4), (8, 2, 4, 8), (8, 2, 8, 4), (8, 4, 4, 4), (8, 4, 4, 6),
 ]
 # per row-tile count: a ragged shape (w not a multiple of 4 where N allows) with V a multiple of 64
 GATHER_VARIANT_SHAPES = {1: (9, 1024, 512, 4, 32, 64), 2: (30, 776, 384, 3, 8, 64),
