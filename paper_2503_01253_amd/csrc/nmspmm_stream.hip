@@ -71,12 +71,19 @@ struct PsShape {
     static constexpr int I = IA + IB + IX;
     static constexpr int CMAX = (I + PS_NL - 1) / PS_NL;         // per loader wave, at most
     // ring depth: NB slots of A_s and B_s and NB+1 of X_s (a stage's offsets
-    // travel with the previous stage) in LDS, at most 6, within the range of
-    // the loaders' vmcnt (NB-2 stages of CMAX instructions in flight)
+    // travel with the previous stage) in LDS, at most NB_MAX, within the range
+    // of the loaders' vmcnt (NB-2 stages of CMAX instructions in flight).  A
+    // shallow ring measured faster than a deep one: more stages in flight
+    // mostly wait in the memory queues (MI355X, graph replay, 4:32:
+    // 512 x 512 x 512 6.98 -> 6.43 us at NB_MAX 6 -> 3, 512 x 1024 x 1024
+    // 9.60 -> 8.63, 512 x 2048 x 2048 15.72 -> 14.97, 1024 x 2048 x 2048
+    // 21.71 -> 21.22; 8:32 and the 8192-wide products unchanged).
+    static constexpr int NB_MAX = 3;
     static constexpr int LDS_FLOATS = 160 * 1024 / 4;
     static constexpr int NB_LDS = (LDS_FLOATS - X_INTS) / (STAGE + X_INTS);
     static constexpr int NB_VM = 2 + 63 / CMAX;
-    static constexpr int NB = NB_LDS < NB_VM ? (NB_LDS < 6 ? NB_LDS : 6) : (NB_VM < 6 ? NB_VM : 6);
+    static constexpr int NB = NB_LDS < NB_VM ? (NB_LDS < NB_MAX ? NB_LDS : NB_MAX) : (NB_VM < NB_MAX ? NB_VM : NB_MAX);
+    static_assert(NB >= 2, "the schedule keeps at least one stage in flight");
     static constexpr int X_BASE = NB * STAGE;           // X_s ring after the A_s / B_s ring
     static constexpr int TOTAL = NB * STAGE + (NB + 1) * X_INTS;
     // split-k epilogue: the tile, staged row-major for coalesced atomics
