@@ -99,6 +99,9 @@ def test_workspace_bytes(monkeypatch):
     MiB = 1 << 20
     assert nm.nmspmm_workspace_bytes(64, 8192, 8192, 4, 32, 64) == 2 * MiB + MiB // 2
     assert nm.nmspmm_workspace_bytes(128, 8192, 8192, 4, 32, 64) == 4 * MiB + MiB // 2
+    # the variants measured fastest on these shapes
+    assert nm.nmspmm_kernel_name_ws(64, 8192, 8192, 4, 32, 64) == "nm_gather_kernel<r64,c32,w8,d4>+prep,split1"
+    assert nm.nmspmm_kernel_name_ws(128, 8192, 8192, 4, 32, 64) == "nm_gather_kernel<r128,c32,w4,d4>+prep,split1"
     # 32 strips of 32 columns, w = 2048: k split 8 ways (8 quads for each of 8 waves)
     assert nm.nmspmm_workspace_bytes(20, 1024, 16384, 4, 32, 64) == 2 * MiB + 16 * 2048 * 4 + 32 * 8 * 32 * 32 * 4
     assert nm.nmspmm_kernel_name_ws(20, 1024, 16384, 4, 32, 64) == "nm_gather_kernel<r32,c32,w8,d4>+prep,split8"
