@@ -193,6 +193,43 @@ NMSPMM_API const char *nmspmm_kernel_name(int64_t m, int64_t n, int64_t k, int N
  * go through the workspace). */
 NMSPMM_API const char *nmspmm_kernel_name_ws(int64_t m, int64_t n, int64_t k, int N, int M, int V);
 
+/* ---- Tuning entry points: for tile sweeps and forced-variant tests only ----
+ * The same product, Eq. 1 as read above, with the kernel choice overridden.
+ * The default entry points above never read overrides (from the environment
+ * or anywhere else); only these three take them, as an explicit string of
+ * "KEY=VALUE" pairs separated by commas (NULL or "" = no override):
+ *   TILE    tile name of the tiled kernel (e.g. "256x256m32w16"), or
+ *           "skinny" for the streaming kernels of short products
+ *   KA      stage depth of the tiled kernel: 32, 64 or 128 columns of A
+ *   SPLITS  workgroups along k (any kernel that splits k)
+ *   RT, SKCOLS, QPW            row tiles, columns per workgroup, quads per
+ *                              wave of the register-operand streaming kernel
+ *   PS      0: never the pipelined streaming kernel, 1: wherever it runs
+ *   PSRT, PSBV, PSCPW, PSRB    its row tiles, columns per lane, column groups
+ *                              per wave and ring rows
+ *   GATHER  0: never the direct-gather kernel, 1: wherever it runs
+ *   GCT, GNW, GD               its column tiles, waves and ring depth
+ * A request the kernels cannot honour falls back to another kernel (a
+ * forced tile that does not fit the shape: the general kernel).  An
+ * unknown key or a malformed pair makes the call fail with
+ * NMSPMM_ERR_INVALID_ARG ("invalid" / -1 for the two queries).  Arguments,
+ * layout, asynchrony, workspace rules and errors otherwise as
+ * nmspmm_run_ws. */
+NMSPMM_API nmspmm_status_t nmspmm_run_tuned(const float *A, const float *Bc, const uint8_t *idx,
+                                 float *C, int64_t m, int64_t n, int64_t k, int N,
+                                 int M, int V, float alpha, const float *bias,
+                                 nmspmm_act_t act, void *workspace, size_t workspace_bytes,
+                                 const char *tuning, hipStream_t stream);
+
+/* nmspmm_kernel_name (with_workspace == 0) or nmspmm_kernel_name_ws
+ * (otherwise) under the overrides of `tuning`. */
+NMSPMM_API const char *nmspmm_kernel_name_tuned(int64_t m, int64_t n, int64_t k, int N, int M, int V,
+                                     int with_workspace, const char *tuning);
+
+/* nmspmm_workspace_bytes under the overrides of `tuning`. */
+NMSPMM_API int64_t nmspmm_workspace_bytes_tuned(int64_t m, int64_t n, int64_t k, int N, int M, int V,
+                                     const char *tuning);
+
 #ifdef __cplusplus
 }
 #endif

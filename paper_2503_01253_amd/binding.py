@@ -28,6 +28,7 @@ EXPORTS = (
     "nmspmm_bc_elems", "nmspmm_idx_bytes", "nmspmm_compress", "nmspmm_compress_device",
     "nmspmm_run", "nmspmm_run_ex", "nmspmm_run_ws", "nmspmm_workspace_bytes", "nmspmm_validate_idx",
     "nmspmm_status_string", "nmspmm_kernel_name", "nmspmm_kernel_name_ws",
+    "nmspmm_run_tuned", "nmspmm_kernel_name_tuned", "nmspmm_workspace_bytes_tuned",
 )
 
 
@@ -77,6 +78,13 @@ def lib():
     L.nmspmm_run_ws.restype = I
     L.nmspmm_workspace_bytes.argtypes = [I64, I64, I64, I, I, I]
     L.nmspmm_workspace_bytes.restype = I64
+    L.nmspmm_run_tuned.argtypes = [P, P, P, P, I64, I64, I64, I, I, I, ctypes.c_float, P, I, P,
+                                   ctypes.c_size_t, ctypes.c_char_p, P]
+    L.nmspmm_run_tuned.restype = I
+    L.nmspmm_kernel_name_tuned.argtypes = [I64, I64, I64, I, I, I, I, ctypes.c_char_p]
+    L.nmspmm_kernel_name_tuned.restype = ctypes.c_char_p
+    L.nmspmm_workspace_bytes_tuned.argtypes = [I64, I64, I64, I, I, I, ctypes.c_char_p]
+    L.nmspmm_workspace_bytes_tuned.restype = I64
     _lib = L
     return L
 
@@ -98,11 +106,26 @@ def nmspmm_idx_bytes(k: int, n: int, N: int, M: int, V: int) -> int:
     return int(lib().nmspmm_idx_bytes(k, n, N, M, V))
 
 
-def nmspmm_kernel_name(m: int, n: int, k: int, N: int, M: int, V: int) -> str:
+def tuning_string(tuning) -> bytes | None:
+    """The tuning overrides of the *_tuned entry points as the library's
+    "KEY=VALUE,..." string (a dict or a string; None or empty: no override).
+    For tile sweeps and forced-variant tests only."""
+    if not tuning:
+        return None
+    if isinstance(tuning, dict):
+        tuning = ",".join(f"{k}={v}" for k, v in tuning.items())
+    return tuning.encode()
+
+
+def nmspmm_kernel_name(m: int, n: int, k: int, N: int, M: int, V: int, tuning=None) -> str:
+    if tuning:
+        return lib().nmspmm_kernel_name_tuned(m, n, k, N, M, V, 0, tuning_string(tuning)).decode()
     return lib().nmspmm_kernel_name(m, n, k, N, M, V).decode()
 
 
-def nmspmm_kernel_name_ws(m: int, n: int, k: int, N: int, M: int, V: int) -> str:
+def nmspmm_kernel_name_ws(m: int, n: int, k: int, N: int, M: int, V: int, tuning=None) -> str:
+    if tuning:
+        return lib().nmspmm_kernel_name_tuned(m, n, k, N, M, V, 1, tuning_string(tuning)).decode()
     return lib().nmspmm_kernel_name_ws(m, n, k, N, M, V).decode()
 
 
@@ -148,34 +171,37 @@ def _check_tensors(torch, C, specs):
             raise ValueError(f"{name} has {t.numel()} elements, expected {numel}")
 
 
-def nmspmm_run(A, Bc, idx, C, m: int, n: int, k: int, N: int, M: int, V: int, stream=None):
+def nmspmm_run(A, Bc, idx, C, m: int, n: int, k: int, N: int, M: int, V: int, stream=None, tuning=None):
     """C = A * B_pruned on the GPU, asynchronously on ``stream`` (a
     torch.cuda.Stream; default: torch's current stream).  A (m x k), Bc
     (w x n), C (m x n) are contiguous fp32 CUDA tensors, idx (w x q) a
-    contiguous uint8 CUDA tensor, all on one device."""
-    return nmspmm_run_ex(A, Bc, idx, C, m, n, k, N, M, V, stream=stream, _name="nmspmm_run")
+    contiguous uint8 CUDA tensor, all on one device.  ``tuning`` (sweeps and
+    tests only) routes the call through nmspmm_run_tuned."""
+    return nmspmm_run_ex(A, Bc, idx, C, m, n, k, N, M, V, stream=stream, tuning=tuning, _name="nmspmm_run")
 
 
-def nmspmm_workspace_bytes(m: int, n: int, k: int, N: int, M: int, V: int) -> int:
+def nmspmm_workspace_bytes(m: int, n: int, k: int, N: int, M: int, V: int, tuning=None) -> int:
     """Workspace bytes nmspmm_run_ws can use for this shape (0: none; -1: bad shape)."""
+    if tuning:
+        return int(lib().nmspmm_workspace_bytes_tuned(m, n, k, N, M, V, tuning_string(tuning)))
     return int(lib().nmspmm_workspace_bytes(m, n, k, N, M, V))
 
 
 def nmspmm_run_ws(A, Bc, idx, C, m: int, n: int, k: int, N: int, M: int, V: int, workspace,
-                  alpha: float = 1.0, bias=None, act: str = "none", stream=None):
+                  alpha: float = 1.0, bias=None, act: str = "none", stream=None, tuning=None):
     """nmspmm_run_ex with a split-k workspace: a uint8 CUDA tensor of at least
     nmspmm_workspace_bytes bytes, 256-byte aligned (or None, or smaller: the
     call runs as nmspmm_run_ex)."""
-    return nmspmm_run_ex(A, Bc, idx, C, m, n, k, N, M, V, alpha, bias, act, stream,
+    return nmspmm_run_ex(A, Bc, idx, C, m, n, k, N, M, V, alpha, bias, act, stream, tuning=tuning,
                          _name="nmspmm_run_ws", _workspace=workspace)
 
 
 def nmspmm_run_ex(A, Bc, idx, C, m: int, n: int, k: int, N: int, M: int, V: int,
-                  alpha: float = 1.0, bias=None, act: str = "none", stream=None,
+                  alpha: float = 1.0, bias=None, act: str = "none", stream=None, tuning=None,
                   _name: str = "nmspmm_run_ex", _workspace=None):
     """C = act(alpha * (A * B_pruned) + bias) on the GPU (alpha = M/N is Eq. 1's
     factor; bias an n-element fp32 CUDA tensor or None; act "none", "relu" or
-    "gelu").  Tensors and stream as for nmspmm_run."""
+    "gelu").  Tensors and stream as for nmspmm_run; ``tuning`` as there."""
     import torch
     L = lib()
     w = (k // M) * N if M > 0 else 0
@@ -192,7 +218,15 @@ def nmspmm_run_ex(A, Bc, idx, C, m: int, n: int, k: int, N: int, M: int, V: int,
     if stream is None:
         stream = torch.cuda.current_stream(C.device)
     with torch.cuda.device(C.device):
-        if _name == "nmspmm_run":
+        if tuning:
+            st = L.nmspmm_run_tuned(A.data_ptr(), Bc.data_ptr(), idx.data_ptr(), C.data_ptr(),
+                                    m, n, k, N, M, V, float(alpha),
+                                    None if bias is None else bias.data_ptr(), ACTS[act],
+                                    None if _workspace is None else _workspace.data_ptr(),
+                                    0 if _workspace is None else _workspace.numel(),
+                                    tuning_string(tuning), stream.cuda_stream)
+            _name = "nmspmm_run_tuned"
+        elif _name == "nmspmm_run":
             st = L.nmspmm_run(A.data_ptr(), Bc.data_ptr(), idx.data_ptr(), C.data_ptr(),
                               m, n, k, N, M, V, stream.cuda_stream)
         elif _name == "nmspmm_run_ws":

@@ -282,17 +282,67 @@ bool prefer_streaming(int64_t m, int64_t k, int N, int M)
     return m <= 128 || (m <= 1024 && m * w < (int64_t(1) << 19));
 }
 
-int env_int(const char *name, int fallback)  // tuning sweeps only
+// Overrides of the dispatch rules, for tuning sweeps and the forced-variant
+// tests only.  They come from the tuning string of the *_tuned entry points
+// ("KEY=VALUE" pairs separated by commas); the default entry points use none
+// and read no environment.  0 (or -1 for PS and GATHER, null for TILE) means
+// "no override".
+struct Tuning {
+    char tile[24] = {};          // TILE: a tile name, or "skinny" for the streaming kernels
+    int ka = 0;                  // KA: stage depth of the tiled kernel (32, 64, 128)
+    int splits = 0;              // SPLITS: k split of any kernel
+    int qpw = 0, skcols = 0, rt = 0;            // QPW, SKCOLS, RT: register-operand streaming kernel
+    int ps = -1;                 // PS: 0 never the pipelined streaming kernel, 1 wherever it runs
+    int psrt = 0, psbv = 0, pscpw = 0, psrb = 0;  // PSRT, PSBV, PSCPW, PSRB: its variant
+    int gather = -1;             // GATHER: 0 never the direct-gather kernel, 1 wherever it runs
+    int gct = 0, gnw = 0, gd = 0;  // GCT, GNW, GD: its variant
+    const char *tile_or_null() const { return tile[0] ? tile : nullptr; }
+};
+
+const Tuning kNoTuning{};
+
+// Parse a tuning string; false on an unknown key or a malformed pair.
+bool parse_tuning(const char *spec, Tuning &t)
 {
-    const char *v = std::getenv(name);
-    return v ? std::atoi(v) : fallback;
+    t = Tuning{};
+    if (!spec) return true;
+    const char *s = spec;
+    while (*s) {
+        const char *eq = std::strchr(s, '=');
+        if (!eq) return false;
+        const char *end = std::strchr(eq + 1, ',');
+        if (!end) end = eq + std::strlen(eq);
+        const std::size_t klen = (std::size_t)(eq - s), vlen = (std::size_t)(end - eq - 1);
+        char key[16] = {}, val[24] = {};
+        if (klen == 0 || klen >= sizeof key || vlen == 0 || vlen >= sizeof val) return false;
+        std::memcpy(key, s, klen);
+        std::memcpy(val, eq + 1, vlen);
+        if (std::strcmp(key, "TILE") == 0) {
+            std::memcpy(t.tile, val, vlen + 1);
+        } else {
+            char *stop = nullptr;
+            const long v = std::strtol(val, &stop, 10);
+            if (*stop != '\0' || v < -1 || v > (1 << 20)) return false;
+            struct { const char *name; int *field; } const fields[] = {
+                {"KA", &t.ka}, {"SPLITS", &t.splits}, {"QPW", &t.qpw}, {"SKCOLS", &t.skcols},
+                {"RT", &t.rt}, {"PS", &t.ps}, {"PSRT", &t.psrt}, {"PSBV", &t.psbv},
+                {"PSCPW", &t.pscpw}, {"PSRB", &t.psrb}, {"GATHER", &t.gather}, {"GCT", &t.gct},
+                {"GNW", &t.gnw}, {"GD", &t.gd}};
+            bool found = false;
+            for (const auto &f : fields)
+                if (std::strcmp(key, f.name) == 0) { *f.field = (int)v; found = true; }
+            if (!found) return false;
+        }
+        s = *end ? end + 1 : end;
+    }
+    return true;
 }
 
 // Streaming kernel for short products: every Bc value is loaded once per
 // 16 rows of C straight into MFMA operands and the A slice is staged in LDS;
 // k is split across workgroups until the grid has about one workgroup per CU.
 bool plan_skinny(const float *A, const float *Bc, const float *C, int64_t m, int64_t n, int64_t k,
-                 int N, int M, int V, Plan &p)
+                 int N, int M, int V, const Tuning &t, Plan &p)
 {
     if (V % 16 != 0 || M % 4 != 0) return false;
     if (!aligned(A, 16) || !aligned(Bc, 16) || !aligned(C, 16)) return false;
@@ -302,7 +352,7 @@ bool plan_skinny(const float *A, const float *Bc, const float *C, int64_t m, int
     // 8:32 30 -> 26 us.  Where the 32-row grid would need split-k it
     // measured slower.
     int rt = m >= 512 && ((m + 31) / 32) * ((n + 127) / 128) >= 256 ? 2 : 1;
-    const int fr = env_int("NMSPMM_RT", 0);
+    const int fr = t.rt;
     if (fr == 1 || fr == 2) rt = fr;
     if (M > skinny_chunk_cols(rt)) return false;
     // buffer offsets: the workgroup's rows of A and 4 rows of Bc per resource
@@ -313,7 +363,7 @@ bool plan_skinny(const float *A, const float *Bc, const float *C, int64_t m, int
     // else 128 (and split-k for the rest)
     const int64_t tiles_m = (m + skinny_rows(rt) - 1) / skinny_rows(rt);
     int cols = tiles_m * ((n + 255) / 256) >= 256 ? 256 : 128;
-    const int fc = env_int("NMSPMM_SKCOLS", 0);
+    const int fc = t.skcols;
     if (fc == 32 || fc == 64 || fc == 128 || fc == 256) cols = fc;
     const int bv = std::min(bv_for(16, V), cols / 16);
     const int64_t tiles_n = (n + cols - 1) / cols;
@@ -323,11 +373,11 @@ bool plan_skinny(const float *A, const float *Bc, const float *C, int64_t m, int
     // per wave) per workgroup
     int64_t splits = std::min<int64_t>((256 + ntiles - 1) / ntiles, G * N / 32);
     splits = std::max<int64_t>(1, std::min<int64_t>(splits, 64));
-    const int fs = env_int("NMSPMM_SPLITS", 0);
+    const int fs = t.splits;
     if (fs >= 1) splits = std::min<int64_t>(fs, std::max<int64_t>(G, 1));
     // longer runs per wave when each workgroup walks all of k
     int qpw = splits == 1 && skinny_has(rt, bv, 4, cols) ? 4 : skinny_has(rt, bv, 2, cols) ? 2 : 1;
-    const int fq = env_int("NMSPMM_QPW", 0);
+    const int fq = t.qpw;
     if (skinny_has(rt, bv, fq, cols)) qpw = fq;
     if (!skinny_has(rt, bv, qpw, cols) || ntiles * splits > INT32_MAX) return false;
     p.kind = Kind::Skinny;
@@ -351,7 +401,7 @@ bool plan_skinny(const float *A, const float *Bc, const float *C, int64_t m, int
 // shapes keep the other kernel) and gains nothing at the denser levels.
 // `force` (tuning sweeps and tests) takes it wherever it can run.
 bool plan_stream(const float *A, const float *Bc, const float *C, int64_t m, int64_t n, int64_t k,
-                 int N, int M, int V, bool force, Plan &p)
+                 int N, int M, int V, bool force, const Tuning &t, Plan &p)
 {
     const int KS = stream_stage_cols();
     if (V % 16 != 0 || M % 4 != 0 || M > KS) return false;
@@ -361,7 +411,7 @@ bool plan_stream(const float *A, const float *Bc, const float *C, int64_t m, int
     int rb = 64;
     for (int r : {16, 32, 64})
         if ((KS / M) * N <= r) { rb = r; break; }
-    const int frb = env_int("NMSPMM_PSRB", 0);
+    const int frb = t.psrb;
     if (frb == 16 || frb == 32 || frb == 64) rb = frb;
     if (N > rb) return false;
     if (!force && (rb > 32 || m <= 16)) return false;
@@ -389,12 +439,12 @@ bool plan_stream(const float *A, const float *Bc, const float *C, int64_t m, int
                 break;
             }
     }
-    const int frt = env_int("NMSPMM_PSRT", 0);
+    const int frt = t.psrt;
     if (frt == 1 || frt == 2 || frt == 4) rt = frt;
-    const int fbv = env_int("NMSPMM_PSBV", 0);
+    const int fbv = t.psbv;
     if ((fbv == 1 || fbv == 2 || fbv == 4) && V % (16 * fbv) == 0) bv = fbv;
     int cpw = 1;
-    const int fcp = env_int("NMSPMM_PSCPW", 0);
+    const int fcp = t.pscpw;
     if (fcp == 1 || fcp == 2) cpw = fcp;
     if (!stream_has(rt, bv, cpw, rb)) return false;
     if ((int64_t)stream_rows(rt) * k * 4 >= (int64_t(1) << 31)) return false;
@@ -407,7 +457,7 @@ bool plan_stream(const float *A, const float *Bc, const float *C, int64_t m, int
     int64_t splits = 1;
     if (fill_splits)   // at least two stages per workgroup
         splits = std::max<int64_t>(1, std::min<int64_t>({(256 + tiles - 1) / tiles, nstages / 2, 64}));
-    const int fs = env_int("NMSPMM_SPLITS", 0);
+    const int fs = t.splits;
     if (fs >= 1) splits = std::min<int64_t>(fs, std::max<int64_t>(G, 1));
     if (tiles * splits > INT32_MAX) return false;
     p.kind = Kind::Stream;
@@ -424,19 +474,19 @@ bool plan_stream(const float *A, const float *Bc, const float *C, int64_t m, int
 }
 
 Plan make_plan(const float *A, const float *Bc, const float *C, int64_t m, int64_t n, int64_t k,
-               int N, int M, int V)
+               int N, int M, int V, const Tuning &t)
 {
     Plan p;
     if (m == 0 || n == 0) return p;
-    const char *force_tile = std::getenv("NMSPMM_TILE");  // tuning sweeps only
+    const char *force_tile = t.tile_or_null();
     const bool want_skinny =
         force_tile ? std::strcmp(force_tile, "skinny") == 0 : prefer_streaming(m, k, N, M);
     if (want_skinny) {
-        // NMSPMM_PS (tuning sweeps and tests): 0 never takes the pipelined
-        // streaming kernel, 1 takes it wherever it can run
-        const int ps = env_int("NMSPMM_PS", -1);
-        if (ps != 0 && plan_stream(A, Bc, C, m, n, k, N, M, V, ps == 1, p)) return p;
-        if (plan_skinny(A, Bc, C, m, n, k, N, M, V, p)) return p;
+        // the PS override (tuning sweeps and tests): 0 never takes the
+        // pipelined streaming kernel, 1 takes it wherever it can run
+        const int ps = t.ps;
+        if (ps != 0 && plan_stream(A, Bc, C, m, n, k, N, M, V, ps == 1, t, p)) return p;
+        if (plan_skinny(A, Bc, C, m, n, k, N, M, V, t, p)) return p;
     }
     p.kind = Kind::General;
     if (k % 4 != 0 || V % 16 != 0 || 128 % M != 0) return p;
@@ -460,7 +510,7 @@ Plan make_plan(const float *A, const float *Bc, const float *C, int64_t m, int64
     };
     int ka_order[3], ka_small[3];
     int nka = ka_list(16, ka_order), nks = ka_list(8, ka_small);
-    const int ka_force = env_int("NMSPMM_KA", 0);
+    const int ka_force = t.ka;
     if (ka_force == 32 || ka_force == 64 || ka_force == 128) {
         ka_order[0] = ka_small[0] = ka_force;
         nka = nks = 1;
@@ -510,10 +560,7 @@ Plan make_plan(const float *A, const float *Bc, const float *C, int64_t m, int64
     int64_t splits = 1;
     if (ntiles < target && stages > 1)
         splits = std::min<int64_t>({(target + ntiles - 1) / ntiles, stages, 32});
-    if (const char *force = std::getenv("NMSPMM_SPLITS")) {  // tuning sweeps only
-        const int64_t s = std::atoll(force);
-        if (s >= 1) splits = std::min<int64_t>(s, std::max<int64_t>(stages, 1));
-    }
+    if (t.splits >= 1) splits = std::min<int64_t>(t.splits, std::max<int64_t>(stages, 1));
     p.kind = Kind::Tiled;
     p.tile = tile;
     p.BV = BV;
@@ -535,7 +582,7 @@ Plan make_plan(const float *A, const float *Bc, const float *C, int64_t m, int64
 // 128 rows 41.0 -> 33.1; at 16 rows it lost (16.4 against 15.0), and split-k
 // through its partial strips lost everywhere it was tried.
 bool plan_gather(const float *Bc, int64_t m, int64_t n, int64_t k, int N, int M, int V, bool force,
-                 Plan &p)
+                 const Tuning &t, Plan &p)
 {
     if (k == 0 || m > 128 || !aligned(Bc, 16)) return false;
     if (!force && (m <= 16 || !prefer_streaming(m, k, N, M))) return false;
@@ -545,9 +592,9 @@ bool plan_gather(const float *Bc, int64_t m, int64_t n, int64_t k, int N, int M,
     // (64 x 8192 x 8192 at 4:32: D = 8 21.7 us, D = 4 20.1-21.5, D = 2 21.9;
     // 128 rows: D = 8 33.0, D = 4 32.2): more loads in flight mostly queue.
     static const int defaults[9][3] = {{}, {2, 8, 4}, {2, 8, 4}, {}, {2, 8, 4}, {}, {}, {}, {2, 4, 4}};
-    c.CT = env_int("NMSPMM_GCT", defaults[c.RT][0]);
-    c.NW = env_int("NMSPMM_GNW", defaults[c.RT][1]);
-    c.D = env_int("NMSPMM_GD", defaults[c.RT][2]);
+    c.CT = t.gct ? t.gct : defaults[c.RT][0];
+    c.NW = t.gnw ? t.gnw : defaults[c.RT][1];
+    c.D = t.gd ? t.gd : defaults[c.RT][2];
     if (!gather_has(c) || V % (16 * c.CT) != 0) return false;
     const int64_t w = (k / M) * N, strips = n / (16 * c.CT);
     const int64_t nquads = (w + 3) / 4;
@@ -559,7 +606,7 @@ bool plan_gather(const float *Bc, int64_t m, int64_t n, int64_t k, int N, int M,
     int64_t splits = 1;
     if (strips < 256)
         splits = std::max<int64_t>(1, std::min<int64_t>((256 + strips - 1) / strips, nquads / (8 * c.NW)));
-    const int fs = env_int("NMSPMM_SPLITS", 0);
+    const int fs = t.splits;
     if (fs >= 1) splits = std::min<int64_t>(fs, std::max<int64_t>(nquads, 1));
     if (strips * splits > INT32_MAX) return false;
     p.kind = Kind::Gather;
@@ -575,17 +622,17 @@ bool plan_gather(const float *Bc, int64_t m, int64_t n, int64_t k, int N, int M,
     return true;
 }
 
-// The plan of a call that brings a workspace.  NMSPMM_GATHER (tuning sweeps
-// and tests): 0 never takes the direct-gather kernel, 1 takes it wherever it
-// can run.
+// The plan of a call that brings a workspace.  The GATHER override (tuning
+// sweeps and tests): 0 never takes the direct-gather kernel, 1 takes it
+// wherever it can run.
 Plan make_ws_plan(const float *A, const float *Bc, const float *C, int64_t m, int64_t n, int64_t k, int N,
-                  int M, int V)
+                  int M, int V, const Tuning &t)
 {
     Plan p;
     if (m == 0 || n == 0) return p;
-    const int g = env_int("NMSPMM_GATHER", -1);
-    if (g != 0 && plan_gather(Bc, m, n, k, N, M, V, g == 1, p)) return p;
-    return make_plan(A, Bc, C, m, n, k, N, M, V);
+    const int g = t.gather;
+    if (g != 0 && plan_gather(Bc, m, n, k, N, M, V, g == 1, t, p)) return p;
+    return make_plan(A, Bc, C, m, n, k, N, M, V, t);
 }
 
 hipError_t launch_general(const float *A, const float *Bc, const uint8_t *idx, float *C,
@@ -776,27 +823,34 @@ const char *plan_name(const Plan &p, bool with_ws)
 
 }  // namespace
 
-extern "C" const char *nmspmm_kernel_name(int64_t m, int64_t n, int64_t k, int N, int M, int V)
+extern "C" const char *nmspmm_kernel_name_tuned(int64_t m, int64_t n, int64_t k, int N, int M, int V,
+                                                int with_workspace, const char *tuning)
 {
-    if (!shape_ok(m, n, k, N, M, V) || !sizes_fit(m, n, k)) return "invalid";
+    Tuning t;
+    if (!parse_tuning(tuning, t) || !shape_ok(m, n, k, N, M, V) || !sizes_fit(m, n, k)) return "invalid";
     // assume buffers as aligned as the allocator returns them
     alignas(64) static const float probe[16] = {};
-    return plan_name(make_plan(probe, probe, probe, m, n, k, N, M, V), false);
+    if (with_workspace) return plan_name(make_ws_plan(probe, probe, probe, m, n, k, N, M, V, t), true);
+    return plan_name(make_plan(probe, probe, probe, m, n, k, N, M, V, t), false);
+}
+
+extern "C" const char *nmspmm_kernel_name(int64_t m, int64_t n, int64_t k, int N, int M, int V)
+{
+    return nmspmm_kernel_name_tuned(m, n, k, N, M, V, 0, nullptr);
 }
 
 extern "C" const char *nmspmm_kernel_name_ws(int64_t m, int64_t n, int64_t k, int N, int M, int V)
 {
-    if (!shape_ok(m, n, k, N, M, V) || !sizes_fit(m, n, k)) return "invalid";
-    alignas(64) static const float probe[16] = {};
-    return plan_name(make_ws_plan(probe, probe, probe, m, n, k, N, M, V), true);
+    return nmspmm_kernel_name_tuned(m, n, k, N, M, V, 1, nullptr);
 }
 
 namespace nmspmm {
 namespace {
 
-nmspmm_status_t run_impl(const float *A, const float *Bc, const uint8_t *idx, float *C, int64_t m, int64_t n,
-                         int64_t k, int N, int M, int V, float alpha, const float *bias, nmspmm_act_t act,
-                         void *workspace, size_t ws_bytes, hipStream_t stream)
+// Argument checks of every product entry point (NMSPMM_OK: go on; m == 0 or
+// n == 0 then means nothing to launch).
+nmspmm_status_t check_run_args(const float *A, const float *Bc, const uint8_t *idx, const float *C, int64_t m,
+                               int64_t n, int64_t k, int N, int M, int V, const float *bias, nmspmm_act_t act)
 {
     if (!shape_ok(m, n, k, N, M, V)) return NMSPMM_ERR_INVALID_ARG;
     if (act != NMSPMM_ACT_NONE && act != NMSPMM_ACT_RELU && act != NMSPMM_ACT_GELU)
@@ -807,11 +861,20 @@ nmspmm_status_t run_impl(const float *A, const float *Bc, const uint8_t *idx, fl
     if (k > 0 && (!A || !Bc || !idx)) return NMSPMM_ERR_INVALID_ARG;
     if (!aligned(C, 4) || (k > 0 && (!aligned(A, 4) || !aligned(Bc, 4))) || !aligned(bias, 4))
         return NMSPMM_ERR_UNSUPPORTED;
+    return NMSPMM_OK;
+}
+
+nmspmm_status_t run_impl(const float *A, const float *Bc, const uint8_t *idx, float *C, int64_t m, int64_t n,
+                         int64_t k, int N, int M, int V, float alpha, const float *bias, nmspmm_act_t act,
+                         void *workspace, size_t ws_bytes, const Tuning &t, hipStream_t stream)
+{
+    const nmspmm_status_t st = check_run_args(A, Bc, idx, C, m, n, k, N, M, V, bias, act);
+    if (st != NMSPMM_OK || m == 0 || n == 0) return st;
     if (workspace && !aligned(workspace, 256)) return NMSPMM_ERR_UNSUPPORTED;
     // with a workspace large enough for it, the plan of nmspmm_workspace_bytes;
     // otherwise that of a call without one
-    Plan p = workspace ? make_ws_plan(A, Bc, C, m, n, k, N, M, V) : make_plan(A, Bc, C, m, n, k, N, M, V);
-    if (workspace && (uint64_t)plan_ws_bytes(p) > (uint64_t)ws_bytes) p = make_plan(A, Bc, C, m, n, k, N, M, V);
+    Plan p = workspace ? make_ws_plan(A, Bc, C, m, n, k, N, M, V, t) : make_plan(A, Bc, C, m, n, k, N, M, V, t);
+    if (workspace && (uint64_t)plan_ws_bytes(p) > (uint64_t)ws_bytes) p = make_plan(A, Bc, C, m, n, k, N, M, V, t);
     if (p.kind == Kind::None) return NMSPMM_OK;
     Epilogue epi;
     epi.alpha = alpha;
@@ -831,7 +894,7 @@ extern "C" nmspmm_status_t nmspmm_run_ex(const float *A, const float *Bc, const 
                                          int V, float alpha, const float *bias, nmspmm_act_t act,
                                          hipStream_t stream)
 {
-    return run_impl(A, Bc, idx, C, m, n, k, N, M, V, alpha, bias, act, nullptr, 0, stream);
+    return run_impl(A, Bc, idx, C, m, n, k, N, M, V, alpha, bias, act, nullptr, 0, kNoTuning, stream);
 }
 
 extern "C" nmspmm_status_t nmspmm_run_ws(const float *A, const float *Bc, const uint8_t *idx,
@@ -839,16 +902,34 @@ extern "C" nmspmm_status_t nmspmm_run_ws(const float *A, const float *Bc, const 
                                          int V, float alpha, const float *bias, nmspmm_act_t act,
                                          void *workspace, size_t workspace_bytes, hipStream_t stream)
 {
-    return run_impl(A, Bc, idx, C, m, n, k, N, M, V, alpha, bias, act, workspace, workspace_bytes, stream);
+    return run_impl(A, Bc, idx, C, m, n, k, N, M, V, alpha, bias, act, workspace, workspace_bytes, kNoTuning,
+                    stream);
+}
+
+extern "C" nmspmm_status_t nmspmm_run_tuned(const float *A, const float *Bc, const uint8_t *idx, float *C,
+                                            int64_t m, int64_t n, int64_t k, int N, int M, int V, float alpha,
+                                            const float *bias, nmspmm_act_t act, void *workspace,
+                                            size_t workspace_bytes, const char *tuning, hipStream_t stream)
+{
+    Tuning t;
+    if (!parse_tuning(tuning, t)) return NMSPMM_ERR_INVALID_ARG;
+    return run_impl(A, Bc, idx, C, m, n, k, N, M, V, alpha, bias, act, workspace, workspace_bytes, t, stream);
+}
+
+extern "C" int64_t nmspmm_workspace_bytes_tuned(int64_t m, int64_t n, int64_t k, int N, int M, int V,
+                                                const char *tuning)
+{
+    Tuning t;
+    if (!parse_tuning(tuning, t) || !shape_ok(m, n, k, N, M, V) || !sizes_fit(m, n, k)) return -1;
+    if (m == 0 || n == 0) return 0;
+    // buffers aligned as the allocator returns them
+    alignas(64) static const float probe[16] = {};
+    return plan_ws_bytes(make_ws_plan(probe, probe, probe, m, n, k, N, M, V, t));
 }
 
 extern "C" int64_t nmspmm_workspace_bytes(int64_t m, int64_t n, int64_t k, int N, int M, int V)
 {
-    if (!shape_ok(m, n, k, N, M, V) || !sizes_fit(m, n, k)) return -1;
-    if (m == 0 || n == 0) return 0;
-    // buffers aligned as the allocator returns them
-    alignas(64) static const float probe[16] = {};
-    return plan_ws_bytes(make_ws_plan(probe, probe, probe, m, n, k, N, M, V));
+    return nmspmm_workspace_bytes_tuned(m, n, k, N, M, V, nullptr);
 }
 
 extern "C" nmspmm_status_t nmspmm_run(const float *A, const float *Bc, const uint8_t *idx,
@@ -857,3 +938,4 @@ extern "C" nmspmm_status_t nmspmm_run(const float *A, const float *Bc, const uin
 {
     return nmspmm_run_ex(A, Bc, idx, C, m, n, k, N, M, V, 1.f, nullptr, NMSPMM_ACT_NONE, stream);
 }
+

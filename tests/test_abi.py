@@ -22,12 +22,37 @@ def declared_symbols():
 
 def test_library_exports_every_declared_symbol():
     names = declared_symbols()
-    assert len(names) == 12
+    assert len(names) == 15
     assert sorted(nm.EXPORTS) == names
     L = nm.lib()
     for name in names:
         assert hasattr(L, name), name
         assert ctypes.cast(getattr(L, name), ctypes.c_void_p).value
+
+
+def test_default_dispatch_reads_no_environment(monkeypatch):
+    """The default entry points ignore tuning-looking environment variables;
+    overrides reach the library only through the *_tuned calls."""
+    shape = (4096, 4096, 4096, 16, 32, 32)
+    before = nm.nmspmm_kernel_name(*shape), nm.nmspmm_kernel_name_ws(*shape), nm.nmspmm_workspace_bytes(*shape)
+    for key, val in (("TILE", "128x128"), ("SPLITS", "4"), ("KA", "64"), ("GATHER", "1"), ("PS", "1")):
+        monkeypatch.setenv("NMSPMM_" + key, val)
+    assert (nm.nmspmm_kernel_name(*shape), nm.nmspmm_kernel_name_ws(*shape),
+            nm.nmspmm_workspace_bytes(*shape)) == before
+    forced = nm.nmspmm_kernel_name(*shape, tuning={"TILE": "128x128", "SPLITS": 4, "KA": 32})
+    assert forced.startswith("nm_tiled_kernel<128x128,") and ",ka32," in forced and forced.endswith("split4")
+
+
+def test_tuning_string_is_checked():
+    L = nm.lib()
+    shape = (4096, 4096, 4096, 16, 32, 32)
+    for bad in (b"FOO=1", b"KA", b"KA=x", b"=3", b"KA=64,,", b"TILE=" + b"x" * 40):
+        assert L.nmspmm_kernel_name_tuned(*shape, 0, bad) == b"invalid", bad
+        assert L.nmspmm_workspace_bytes_tuned(*shape, bad) == -1, bad
+        assert L.nmspmm_run_tuned(0, 0, 0, 0, *shape[:0], 8, 64, 64, 4, 32, 32, ctypes.c_float(1.0), None, 0,
+                                  None, 0, bad, None) == nm.NMSPMM_ERR_INVALID_ARG, bad
+    assert L.nmspmm_kernel_name_tuned(*shape, 0, b"") == nm.nmspmm_kernel_name(*shape).encode()
+    assert L.nmspmm_kernel_name_tuned(*shape, 0, None) == nm.nmspmm_kernel_name(*shape).encode()
 
 
 def test_size_helpers():
@@ -89,7 +114,7 @@ def test_validate_idx_rejects_broken_patterns():
     assert nm.nmspmm_validate_idx(idx, k + 1, n, N, M, V) == nm.NMSPMM_ERR_INVALID_ARG
 
 
-def test_workspace_bytes(monkeypatch):
+def test_workspace_bytes():
     """Workspace sizes (host only); -1 for a bad shape.  Short products with V
     a multiple of 32 take the direct-gather kernel: a transposed copy of A
     (k x 16, 32, 64 or 128 floats), the offsets (4 * w * n/V bytes) and, when
@@ -107,19 +132,18 @@ def test_workspace_bytes(monkeypatch):
     assert nm.nmspmm_kernel_name_ws(20, 1024, 16384, 4, 32, 64) == "nm_gather_kernel<r32,c32,w8,d4>+prep,split8"
     # 16 rows keep the register-operand streaming kernel (atomics, no workspace)
     assert nm.nmspmm_workspace_bytes(16, 8192, 8192, 4, 32, 64) == 0
-    monkeypatch.setenv("NMSPMM_GATHER", "1")
-    assert nm.nmspmm_workspace_bytes(16, 8192, 8192, 4, 32, 64) == MiB // 2 + MiB // 2
-    monkeypatch.delenv("NMSPMM_GATHER")
+    assert nm.nmspmm_workspace_bytes(16, 8192, 8192, 4, 32, 64, tuning={"GATHER": 1}) == MiB // 2 + MiB // 2
     assert nm.nmspmm_workspace_bytes(4096, 4096, 4096, 16, 32, 32) == 0    # tiled, no split
     assert nm.nmspmm_workspace_bytes(512, 2048, 2048, 4, 32, 32) == 0      # no split
     assert nm.nmspmm_workspace_bytes(0, 64, 64, 4, 32, 32) == 0
     assert nm.nmspmm_workspace_bytes(10, 64, 65, 4, 32, 32) == -1
-    monkeypatch.setenv("NMSPMM_GATHER", "0")
+    no_gather = {"GATHER": 0}
     # 16 x 8192 x 8192 at 4:32: register-operand streaming kernel, atomics
-    assert nm.nmspmm_workspace_bytes(16, 8192, 8192, 4, 32, 64) == 0
+    assert nm.nmspmm_workspace_bytes(16, 8192, 8192, 4, 32, 64, tuning=no_gather) == 0
     # 64 x 8192 x 8192: pipelined streaming kernel, 64 tiles of 32 x 256, split 4
-    assert nm.nmspmm_workspace_bytes(64, 8192, 8192, 4, 32, 64) == 64 * 4 * 32 * 256 * 4
-    assert nm.nmspmm_kernel_name_ws(64, 8192, 8192, 4, 32, 64) == "nm_stream_kernel<r32,c256,bv2,rb16>+ws,split4"
+    assert nm.nmspmm_workspace_bytes(64, 8192, 8192, 4, 32, 64, tuning=no_gather) == 64 * 4 * 32 * 256 * 4
+    assert nm.nmspmm_kernel_name_ws(64, 8192, 8192, 4, 32, 64, tuning=no_gather) == \
+        "nm_stream_kernel<r32,c256,bv2,rb16>+ws,split4"
 
 
 def test_run_ws_rejects_misaligned_workspace_before_any_launch():

@@ -29,25 +29,49 @@ def to_dev(x):
     return torch.from_numpy(np.ascontiguousarray(x)).cuda()
 
 
+# Kernel overrides of the current test (the library's tuning entry points:
+# forced variants), cleared before every test; empty = the default dispatch.
+TUNE = {}
+
+
+@pytest.fixture(autouse=True)
+def _clear_tuning():
+    TUNE.clear()
+    yield
+    TUNE.clear()
+
+
+def kname(m, n, k, N, M, V):
+    return nm.nmspmm_kernel_name(m, n, k, N, M, V, tuning=TUNE)
+
+
+def kname_ws(m, n, k, N, M, V):
+    return nm.nmspmm_kernel_name_ws(m, n, k, N, M, V, tuning=TUNE)
+
+
+def ws_bytes(m, n, k, N, M, V):
+    return nm.nmspmm_workspace_bytes(m, n, k, N, M, V, tuning=TUNE)
+
+
 def gpu_run(A, Bc, idx, m, n, k, N, M, V, stream=None, fill=float("nan"), workspace=False):
     """Run the library on host arrays; C starts as NaN so unwritten outputs
     fail.  workspace=True: nmspmm_run_ws with a workspace of the size the
     shape takes (the launch the benchmark times)."""
     dA, dBc, didx = to_dev(A), to_dev(Bc), to_dev(idx)
     dC = torch.full((m, n), fill, dtype=torch.float32, device="cuda")
-    need = nm.nmspmm_workspace_bytes(m, n, k, N, M, V) if workspace else 0
+    need = ws_bytes(m, n, k, N, M, V) if workspace else 0
     if need > 0:
         ws = torch.full((need,), 0xFF, dtype=torch.uint8, device="cuda")
-        nm.nmspmm_run_ws(dA, dBc, didx, dC, m, n, k, N, M, V, ws, stream=stream)
+        nm.nmspmm_run_ws(dA, dBc, didx, dC, m, n, k, N, M, V, ws, stream=stream, tuning=TUNE)
     else:
-        nm.nmspmm_run(dA, dBc, didx, dC, m, n, k, N, M, V, stream=stream)
+        nm.nmspmm_run(dA, dBc, didx, dC, m, n, k, N, M, V, stream=stream, tuning=TUNE)
     torch.cuda.synchronize()
     return dC.cpu().numpy()
 
 
 def parity(m, k, n, N, M, V, dist, seed):
     say(f"[parity] m={m} k={k} n={n} {N}:{M} V={V} {dist} seed={seed} "
-        f"kernel={nm.nmspmm_kernel_name(m, n, k, N, M, V)}")
+        f"kernel={kname(m, n, k, N, M, V)}")
     A, Bp, _ = make_inputs(m, k, n, N, M, V, seed, dist)
     Bc, idx = nm.nmspmm_compress(Bp, N, M, V)
     Bc_o, idx_o = oracle.compress(Bp, N, M, V)
@@ -115,51 +139,39 @@ def test_small_integers_exact(shape):
         f"{int(np.count_nonzero(C.astype(np.float64) != C_ref))} outputs differ"
 
 
-@pytest.mark.parametrize("name", list(RUNS))
-def test_parity_full_size_sampled_rows(name):
-    """Each benchmark workload at full size, in the launch the benchmark times;
-    the oracle computes a sample of rows (first, last, tile edges, random)."""
-    run = RUNS[name]
+def full_parity(run, tag):
+    """One workload at full size, in the launch the benchmark times (with the
+    workspace where the shape takes one): the library's packer must equal the
+    oracle's byte for byte, and every output element is compared with the
+    oracle's fp64 product at the bar."""
     m, k, n, N, M, V = run.m, run.k, run.n, run.N, run.M, run.V
-    say(f"[full] {run.describe()} kernel={nm.nmspmm_kernel_name_ws(m, n, k, N, M, V)}")
+    say(f"[{tag}] {run.describe()} kernel={kname_ws(m, n, k, N, M, V)}")
     A, Bp, _ = make_run(run)
     Bc, idx = nm.nmspmm_compress(Bp, N, M, V)
-    C = gpu_run(A, Bc, idx, m, n, k, N, M, V, workspace=True)
-    assert np.isfinite(C).all()
-    rng = np.random.default_rng(run.seed)
-    rows = {0, m - 1, min(m - 1, 127), min(m - 1, 128), min(m - 1, 255), min(m - 1, 256)}
-    rows |= set(int(x) for x in rng.integers(0, m, size=8))
-    rows = np.array(sorted(rows))
     Bc_o, idx_o = oracle.compress(Bp, N, M, V)
-    assert np.array_equal(idx, idx_o) and np.array_equal(Bc, Bc_o)
-    As = np.ascontiguousarray(A[rows])
-    C_ref = oracle.spmm(As, Bc_o, idx_o, len(rows), n, k, N, M, V)
-    Bnd = oracle.bound(As, Bc_o, idx_o, len(rows), n, k, N, M, V)
-    r = oracle.check(C[rows], C_ref, Bnd)
-    say(f"[full] {name}: {r}")
+    assert np.array_equal(idx, idx_o) and Bc.tobytes() == Bc_o.tobytes()
+    C = gpu_run(A, Bc, idx, m, n, k, N, M, V, workspace=True)
+    r = oracle.check(C, oracle.spmm(A, Bc_o, idx_o, m, n, k, N, M, V),
+                     oracle.bound(A, Bc_o, idx_o, m, n, k, N, M, V))
+    say(f"[{tag}] {run.name}: {r}")
     assert r, r
+
+
+@pytest.mark.parametrize("name", list(RUNS))
+def test_parity_full_size(name):
+    """Each benchmark workload (256^3 to 4096^3, the MLP shape, the 16-128 row
+    decode shapes), every element against the oracle."""
+    full_parity(RUNS[name], "full")
 
 
 TABLE = table_runs()
 
 
 @pytest.mark.parametrize("name", list(TABLE))
-def test_shape_sparsity_table_sampled_rows(name):
-    """Every point of the shape x sparsity sweep (0 % to 87.5 %), in the launch
-    the benchmark times; the oracle computes a sample of rows."""
-    run = TABLE[name]
-    m, k, n, N, M, V = run.m, run.k, run.n, run.N, run.M, run.V
-    say(f"[table] {run.describe()} kernel={nm.nmspmm_kernel_name_ws(m, n, k, N, M, V)}")
-    A, Bp, _ = make_run(run)
-    Bc, idx = nm.nmspmm_compress(Bp, N, M, V)
-    C = gpu_run(A, Bc, idx, m, n, k, N, M, V, workspace=True)
-    assert np.isfinite(C).all()
-    rng = np.random.default_rng(run.seed)
-    rows = np.array(sorted({0, m - 1, 127, 128, 255, 256} | set(int(x) for x in rng.integers(0, m, 6))))
-    As = np.ascontiguousarray(A[rows])
-    r = oracle.check(C[rows], oracle.spmm(As, Bc, idx, len(rows), n, k, N, M, V),
-                     oracle.bound(As, Bc, idx, len(rows), n, k, N, M, V))
-    assert r, r
+def test_shape_sparsity_table_full(name):
+    """Every point of the shape x sparsity sweep (0 % to 87.5 %), every element
+    against the oracle."""
+    full_parity(TABLE[name], "table")
 
 
 def test_k_zero_writes_zeros_and_m_zero_is_noop():
@@ -176,7 +188,7 @@ def test_deterministic_and_stream_ordered():
     """Without split-k (>= 256 tiles) every output is one workgroup's fixed
     MFMA chain: two runs, on different streams, are bitwise identical."""
     m, k, n, N, M, V = 2048, 128, 8192, 8, 32, 32
-    assert nm.nmspmm_kernel_name(m, n, k, N, M, V).endswith(",split1")
+    assert kname(m, n, k, N, M, V).endswith(",split1")
     A, Bp, _ = make_inputs(m, k, n, N, M, V, 99)
     Bc, idx = nm.nmspmm_compress(Bp, N, M, V)
     C1 = gpu_run(A, Bc, idx, m, n, k, N, M, V)
@@ -191,7 +203,7 @@ def test_split_k_runs_agree_within_tolerance():
     """Split-k adds partial tiles with fp32 atomics, so the summation order
     (and the last bits) may vary between runs; both runs meet the bar."""
     m, k, n, N, M, V = 1030, 256, 1088, 8, 32, 32
-    assert "split" in nm.nmspmm_kernel_name(m, n, k, N, M, V)
+    assert "split" in kname(m, n, k, N, M, V)
     A, Bp, _ = make_inputs(m, k, n, N, M, V, 99)
     Bc, idx = nm.nmspmm_compress(Bp, N, M, V)
     C_ref = oracle.spmm(A, Bc, idx, m, n, k, N, M, V)
@@ -202,12 +214,12 @@ def test_split_k_runs_agree_within_tolerance():
 
 
 @pytest.mark.parametrize("scale", [2.0, 4.0, 8.0])
-def test_power_of_two_scaling_is_exact(scale, monkeypatch):
+def test_power_of_two_scaling_is_exact(scale):
     """Eq. 1's M/N factor, applied by the caller to Bc, scales C exactly (one
     workgroup per output tile, so both runs add in the same order)."""
-    monkeypatch.setenv("NMSPMM_SPLITS", "1")
+    TUNE["SPLITS"] = "1"
     m, k, n, N, M, V = 300, 256, 320, 32 // int(scale), 32, 32
-    assert nm.nmspmm_kernel_name(m, n, k, N, M, V).endswith(",split1")
+    assert kname(m, n, k, N, M, V).endswith(",split1")
     A, Bp, _ = make_inputs(m, k, n, N, M, V, 17)
     Bc, idx = nm.nmspmm_compress(Bp, N, M, V)
     C = gpu_run(A, Bc, idx, m, n, k, N, M, V)
@@ -240,12 +252,12 @@ FORCED = [
 
 @pytest.mark.parametrize("tile", TILES)
 @pytest.mark.parametrize("shape", FORCED, ids=lambda s: "x".join(map(str, s)))
-def test_every_tile_shape_exact(tile, shape, monkeypatch):
+def test_every_tile_shape_exact(tile, shape):
     """Each tile shape the dispatcher can pick, forced on ragged problems
     with small-integer data (exact in any summation order)."""
     m, k, n, N, M, V = shape
-    monkeypatch.setenv("NMSPMM_TILE", tile)
-    name = nm.nmspmm_kernel_name(m, n, k, N, M, V)
+    TUNE["TILE"] = tile
+    name = kname(m, n, k, N, M, V)
     if f"<{tile}," not in name and not (tile == "skinny" and name.startswith("nm_skinny")):
         pytest.skip(f"{tile} does not fit {shape} ({name})")
     C, C_ref, _ = parity(m, k, n, N, M, V, "int", seed=7 + m + n)
@@ -266,12 +278,12 @@ ONE_A = [
 @pytest.mark.parametrize("splits", [1, 2])
 @pytest.mark.parametrize("tile", ONE_A_TILES)
 @pytest.mark.parametrize("shape", ONE_A, ids=lambda s: "x".join(map(str, s)))
-def test_single_a_slot_deep_stages(tile, shape, splits, monkeypatch):
+def test_single_a_slot_deep_stages(tile, shape, splits):
     m, k, n, N, M, V = shape
-    monkeypatch.setenv("NMSPMM_TILE", tile)
-    monkeypatch.setenv("NMSPMM_KA", "128")
-    monkeypatch.setenv("NMSPMM_SPLITS", str(splits))
-    name = nm.nmspmm_kernel_name(m, n, k, N, M, V)
+    TUNE["TILE"] = tile
+    TUNE["KA"] = "128"
+    TUNE["SPLITS"] = str(splits)
+    name = kname(m, n, k, N, M, V)
     if tile in ("128x256m32", "128x256m32w16", "128x512m32w16"):
         assert f"<{tile}," in name and ",ka128," in name, name
     elif f"<{tile}," not in name or ",ka128," not in name:
@@ -296,16 +308,16 @@ SKINNY = [
                                       (32, 4), (32, 8)])
 @pytest.mark.parametrize("splits", [1, 3])
 @pytest.mark.parametrize("shape", SKINNY, ids=lambda s: "x".join(map(str, s)))
-def test_skinny_variants_exact(shape, splits, cols, qpw, monkeypatch):
+def test_skinny_variants_exact(shape, splits, cols, qpw):
     """Every streaming-kernel variant (columns per workgroup, quads per wave,
     k split), forced, on small-integer data (exact in any summation order)."""
     m, k, n, N, M, V = shape
-    monkeypatch.setenv("NMSPMM_TILE", "skinny")
-    monkeypatch.setenv("NMSPMM_PS", "0")
-    monkeypatch.setenv("NMSPMM_SKCOLS", str(cols))
-    monkeypatch.setenv("NMSPMM_QPW", str(qpw))
-    monkeypatch.setenv("NMSPMM_SPLITS", str(splits))
-    name = nm.nmspmm_kernel_name(m, n, k, N, M, V)
+    TUNE["TILE"] = "skinny"
+    TUNE["PS"] = "0"
+    TUNE["SKCOLS"] = str(cols)
+    TUNE["QPW"] = str(qpw)
+    TUNE["SPLITS"] = str(splits)
+    name = kname(m, n, k, N, M, V)
     if not name.startswith(f"nm_skinny_kernel<c{cols},") or f"qpw{qpw}>" not in name:
         pytest.skip(f"variant not instantiated for {shape} ({name})")
     C, C_ref, _ = parity(m, k, n, N, M, V, "int", seed=11 + m + n)
@@ -326,18 +338,18 @@ SKINNY32 = [
 @pytest.mark.parametrize("cols,qpw", [(128, 1), (128, 2), (128, 4), (256, 1), (256, 2)])
 @pytest.mark.parametrize("splits", [1, 3])
 @pytest.mark.parametrize("shape", SKINNY32, ids=lambda s: "x".join(map(str, s)))
-def test_skinny_32_row_variants_exact(shape, splits, cols, qpw, monkeypatch):
+def test_skinny_32_row_variants_exact(shape, splits, cols, qpw):
     """The streaming kernel with 32 rows per workgroup, forced, on
     small-integer data (exact in any summation order), and on normal data
     against the bar."""
     m, k, n, N, M, V = shape
-    monkeypatch.setenv("NMSPMM_TILE", "skinny")
-    monkeypatch.setenv("NMSPMM_PS", "0")
-    monkeypatch.setenv("NMSPMM_RT", "2")
-    monkeypatch.setenv("NMSPMM_SKCOLS", str(cols))
-    monkeypatch.setenv("NMSPMM_QPW", str(qpw))
-    monkeypatch.setenv("NMSPMM_SPLITS", str(splits))
-    name = nm.nmspmm_kernel_name(m, n, k, N, M, V)
+    TUNE["TILE"] = "skinny"
+    TUNE["PS"] = "0"
+    TUNE["RT"] = "2"
+    TUNE["SKCOLS"] = str(cols)
+    TUNE["QPW"] = str(qpw)
+    TUNE["SPLITS"] = str(splits)
+    name = kname(m, n, k, N, M, V)
     if not name.startswith(f"nm_skinny_kernel<c{cols},") or f"qpw{qpw},rows32>" not in name:
         pytest.skip(f"variant not instantiated for {shape} ({name})")
     C, C_ref, _ = parity(m, k, n, N, M, V, "int", seed=21 + m + n)
@@ -348,13 +360,13 @@ def test_skinny_32_row_variants_exact(shape, splits, cols, qpw, monkeypatch):
     assert r, (name, r)
 
 
-def test_skinny_32_rows_chosen_for_wide_grids(monkeypatch):
+def test_skinny_32_rows_chosen_for_wide_grids():
     """Without the pipelined kernel, the register-operand streaming kernel
     takes 32-row workgroups where that grid alone fills the chip (512 x 2048
     x 2048 at 4:32), and 16 rows for decode-like shapes."""
-    monkeypatch.setenv("NMSPMM_PS", "0")
-    assert nm.nmspmm_kernel_name(512, 2048, 2048, 4, 32, 32).endswith("rows32>,split1")
-    assert "rows32" not in nm.nmspmm_kernel_name(64, 8192, 8192, 4, 32, 64)
+    TUNE["PS"] = "0"
+    assert kname(512, 2048, 2048, 4, 32, 32).endswith("rows32>,split1")
+    assert "rows32" not in kname(64, 8192, 8192, 4, 32, 64)
 
 
 # ---- pipelined streaming kernel (loader waves, LDS ring) ----
@@ -378,7 +390,7 @@ STREAM_VARIANTS = [(1, 1, 1, 16), (1, 2, 1, 16), (1, 4, 1, 16), (1, 2, 1, 32), (
 @pytest.mark.parametrize("splits", [1, 3])
 @pytest.mark.parametrize("variant", STREAM_VARIANTS, ids=lambda v: "rt%d_bv%d_cpw%d_rb%d" % v)
 @pytest.mark.parametrize("shape", STREAM, ids=lambda s: "x".join(map(str, s)))
-def test_stream_variants_exact(shape, variant, splits, monkeypatch):
+def test_stream_variants_exact(shape, variant, splits):
     """Every instantiation of the pipelined streaming kernel (row tiles,
     columns per lane, column groups per wave, ring rows), forced, on
     small-integer data (exact in any summation order) and on normal data
@@ -387,8 +399,8 @@ def test_stream_variants_exact(shape, variant, splits, monkeypatch):
     rt, bv, cpw, rb = variant
     for key, val in (("PS", 1), ("PSRT", rt), ("PSBV", bv), ("PSCPW", cpw), ("PSRB", rb),
                      ("SPLITS", splits)):
-        monkeypatch.setenv("NMSPMM_" + key, str(val))
-    name = nm.nmspmm_kernel_name(m, n, k, N, M, V)
+        TUNE[key] = str(val)
+    name = kname(m, n, k, N, M, V)
     want = "nm_stream_kernel<r%d,c%d,bv%d,rb%d>" % (16 * rt, 128 * bv * cpw, bv, rb)
     if not name.startswith(want):
         pytest.skip(f"variant not available for {shape} ({name})")
@@ -400,20 +412,20 @@ def test_stream_variants_exact(shape, variant, splits, monkeypatch):
     assert r, (name, r)
 
 
-def test_stream_kernel_chosen_by_rule(monkeypatch):
+def test_stream_kernel_chosen_by_rule():
     """The dispatcher takes the pipelined kernel for the sparse levels (ring of
     16 or 32 rows) above 16 rows: 32-row tiles with split-k for short
     products, the largest tile that fills the chip for taller ones; and keeps
     the register-operand kernel for 16-row decode shapes and denser levels."""
-    monkeypatch.delenv("NMSPMM_PS", raising=False)
-    assert nm.nmspmm_kernel_name(64, 8192, 8192, 4, 32, 64) == "nm_stream_kernel<r32,c256,bv2,rb16>+zero,split4"
-    assert nm.nmspmm_kernel_name(1024, 2048, 2048, 4, 32, 32) == "nm_stream_kernel<r32,c256,bv2,rb16>,split1"
-    assert nm.nmspmm_kernel_name(512, 2048, 2048, 8, 32, 32) == "nm_stream_kernel<r16,c256,bv2,rb32>,split1"
-    assert nm.nmspmm_kernel_name(512, 512, 512, 4, 32, 32) == "nm_stream_kernel<r16,c128,bv1,rb16>,split1"
-    assert nm.nmspmm_kernel_name(16, 8192, 8192, 4, 32, 64).startswith("nm_skinny_kernel")
-    assert nm.nmspmm_kernel_name(512, 1024, 1024, 16, 32, 32).startswith("nm_skinny_kernel")
-    monkeypatch.setenv("NMSPMM_PS", "0")
-    assert nm.nmspmm_kernel_name(64, 8192, 8192, 4, 32, 64).startswith("nm_skinny_kernel")
+    TUNE.pop("PS", None)
+    assert kname(64, 8192, 8192, 4, 32, 64) == "nm_stream_kernel<r32,c256,bv2,rb16>+zero,split4"
+    assert kname(1024, 2048, 2048, 4, 32, 32) == "nm_stream_kernel<r32,c256,bv2,rb16>,split1"
+    assert kname(512, 2048, 2048, 8, 32, 32) == "nm_stream_kernel<r16,c256,bv2,rb32>,split1"
+    assert kname(512, 512, 512, 4, 32, 32) == "nm_stream_kernel<r16,c128,bv1,rb16>,split1"
+    assert kname(16, 8192, 8192, 4, 32, 64).startswith("nm_skinny_kernel")
+    assert kname(512, 1024, 1024, 16, 32, 32).startswith("nm_skinny_kernel")
+    TUNE["PS"] = "0"
+    assert kname(64, 8192, 8192, 4, 32, 64).startswith("nm_skinny_kernel")
 
 
 def test_dense_comparator_is_true_fp32():
@@ -446,7 +458,7 @@ EPI_SHAPES = [
 def run_ex(A, Bc, idx, m, n, k, N, M, V, alpha, bias, act):
     dC = torch.full((m, n), float("nan"), dtype=torch.float32, device="cuda")
     nm.nmspmm_run_ex(to_dev(A), to_dev(Bc), to_dev(idx), dC, m, n, k, N, M, V, alpha=alpha,
-                     bias=None if bias is None else to_dev(bias), act=act)
+                     bias=None if bias is None else to_dev(bias), act=act, tuning=TUNE)
     torch.cuda.synchronize()
     return dC.cpu().numpy()
 
@@ -459,7 +471,7 @@ def test_run_ex_epilogue(shape, act):
     alpha and the activation (|d act| <= 1.13 |d y|), plus fp32 rounding of the
     epilogue itself."""
     m, k, n, N, M, V = shape
-    say(f"[epilogue] {shape} {act} kernel={nm.nmspmm_kernel_name(m, n, k, N, M, V)}")
+    say(f"[epilogue] {shape} {act} kernel={kname(m, n, k, N, M, V)}")
     A, Bp, _ = make_inputs(m, k, n, N, M, V, 40 + m, "normal")
     Bc, idx = oracle.compress(Bp, N, M, V)
     bias = np.random.default_rng(m).standard_normal(n).astype(np.float32)
@@ -511,7 +523,7 @@ WS_CASES = [
 
 
 def new_workspace(m, n, k, N, M, V):
-    need = nm.nmspmm_workspace_bytes(m, n, k, N, M, V)
+    need = ws_bytes(m, n, k, N, M, V)
     assert need > 0
     ws = torch.full((need,), 0xFF, dtype=torch.uint8, device="cuda")   # contents irrelevant (NaN bytes)
     assert ws.data_ptr() % 256 == 0
@@ -521,21 +533,21 @@ def new_workspace(m, n, k, N, M, V):
 def run_ws(A, Bc, idx, m, n, k, N, M, V, ws, alpha=1.0, bias=None, act="none"):
     dC = torch.full((m, n), float("nan"), dtype=torch.float32, device="cuda")
     nm.nmspmm_run_ws(to_dev(A), to_dev(Bc), to_dev(idx), dC, m, n, k, N, M, V, ws, alpha=alpha,
-                     bias=None if bias is None else to_dev(bias), act=act)
+                     bias=None if bias is None else to_dev(bias), act=act, tuning=TUNE)
     torch.cuda.synchronize()
     return dC.cpu().numpy()
 
 
 @pytest.mark.parametrize("shape,env", WS_CASES, ids=["rows16_v16", "rows32", "rows64", "rows16_empty_split"])
-def test_run_ws_split_k(shape, env, monkeypatch):
+def test_run_ws_split_k(shape, env):
     """Split-k through the workspace: bit-exact on small integers (twice in a
     row on one workspace), the epilogue applied once and exactly, normal data
     within the bar and bit-identical between runs."""
     for key, val in env.items():
-        monkeypatch.setenv("NMSPMM_" + key, val)
-    monkeypatch.setenv("NMSPMM_GATHER", "0")
+        TUNE[key] = val
+    TUNE["GATHER"] = "0"
     m, k, n, N, M, V = shape
-    name = nm.nmspmm_kernel_name_ws(m, n, k, N, M, V)
+    name = kname_ws(m, n, k, N, M, V)
     say(f"[workspace] {shape} {name}")
     assert "+ws,split" in name
     ws = new_workspace(m, n, k, N, M, V)
@@ -573,14 +585,14 @@ def test_run_ws_small_or_missing_workspace_runs_as_run_ex():
 
 
 @pytest.mark.parametrize("gather", ["0", "1"])
-def test_run_ws_graph_replay(gather, monkeypatch):
+def test_run_ws_graph_replay(gather):
     """nmspmm_run_ws captured in a HIP graph (two kernels, no fill of C and no
     memset: split-k of the pipelined streaming kernel, or the transposition
     pass and the direct-gather kernel): every replay, with eager work between
     replays, gives the eager result bit for bit."""
-    monkeypatch.setenv("NMSPMM_GATHER", gather)
+    TUNE["GATHER"] = gather
     m, k, n, N, M, V = 64, 2048, 2048, 4, 32, 64
-    name = nm.nmspmm_kernel_name_ws(m, n, k, N, M, V)
+    name = kname_ws(m, n, k, N, M, V)
     say(f"[graph] {name}")
     assert ("+ws,split" if gather == "0" else "nm_gather_kernel") in name
     A, Bp, _ = make_inputs(m, k, n, N, M, V, 78, "normal")
@@ -590,12 +602,12 @@ def test_run_ws_graph_replay(gather, monkeypatch):
     dC = torch.empty((m, n), dtype=torch.float32, device="cuda")
     s = torch.cuda.Stream()
     with torch.cuda.stream(s):
-        nm.nmspmm_run_ws(dA, dBc, didx, dC, m, n, k, N, M, V, ws)
+        nm.nmspmm_run_ws(dA, dBc, didx, dC, m, n, k, N, M, V, ws, tuning=TUNE)
     torch.cuda.synchronize()
     eager = dC.cpu().numpy().copy()
     g = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g):
-        nm.nmspmm_run_ws(dA, dBc, didx, dC, m, n, k, N, M, V, ws)
+        nm.nmspmm_run_ws(dA, dBc, didx, dC, m, n, k, N, M, V, ws, tuning=TUNE)
     for i in range(3):
         dC.fill_(float("nan"))
         torch.cuda.synchronize()
@@ -622,15 +634,15 @@ GATHER_SHAPES = [
 
 @pytest.mark.parametrize("splits", ["auto", "3"])
 @pytest.mark.parametrize("shape", GATHER_SHAPES, ids=lambda s: "x".join(map(str, s)))
-def test_gather_kernel_exact(shape, splits, monkeypatch):
+def test_gather_kernel_exact(shape, splits):
     """The direct-gather kernel (forced), with and without split-k: bit-exact on
     small integers twice in a row on one workspace, the epilogue applied once
     and exactly, normal data within the bar and bit-identical between runs."""
-    monkeypatch.setenv("NMSPMM_GATHER", "1")
+    TUNE["GATHER"] = "1"
     if splits != "auto":
-        monkeypatch.setenv("NMSPMM_SPLITS", splits)
+        TUNE["SPLITS"] = splits
     m, k, n, N, M, V = shape
-    name = nm.nmspmm_kernel_name_ws(m, n, k, N, M, V)
+    name = kname_ws(m, n, k, N, M, V)
     say(f"[gather] {shape} {name}")
     assert name.startswith("nm_gather_kernel<r%d," % (16 if m <= 16 else 32 if m <= 32 else 64 if m <= 64 else 128))
     w = k // M * N
@@ -670,14 +682,14 @@ GATHER_VARIANT_SHAPES = {1: (9, 1024, 512, 4, 32, 64), 2: (30, 776, 384, 3, 8, 6
 
 @pytest.mark.parametrize("splits", [1, 3])
 @pytest.mark.parametrize("variant", GATHER_VARIANTS, ids=lambda v: "rt%d_ct%d_nw%d_d%d" % v)
-def test_gather_variants_exact(variant, splits, monkeypatch):
+def test_gather_variants_exact(variant, splits):
     """Every direct-gather instantiation, forced, with and without split-k:
     bit-exact on small integers and within the bar on normal data."""
     rt, ct, nw, d = variant
     for key, val in (("GATHER", 1), ("GCT", ct), ("GNW", nw), ("GD", d), ("SPLITS", splits)):
-        monkeypatch.setenv("NMSPMM_" + key, str(val))
+        TUNE[key] = str(val)
     m, k, n, N, M, V = GATHER_VARIANT_SHAPES[rt]
-    name = nm.nmspmm_kernel_name_ws(m, n, k, N, M, V)
+    name = kname_ws(m, n, k, N, M, V)
     say(f"[gather variant] {variant} split{splits} {name}")
     assert name == f"nm_gather_kernel<r{16 * rt},c{16 * ct},w{nw},d{d}>+prep,split{splits}"
     ws = new_workspace(m, n, k, N, M, V)
@@ -692,13 +704,13 @@ def test_gather_variants_exact(variant, splits, monkeypatch):
     assert r, (name, r)
 
 
-def test_gather_kernel_reused_workspace_smaller_shape(monkeypatch):
+def test_gather_kernel_reused_workspace_smaller_shape():
     """One workspace, a large call then a smaller one of another row count: the
     second call's transposed copy and offsets replace the first's."""
-    monkeypatch.setenv("NMSPMM_GATHER", "1")
+    TUNE["GATHER"] = "1"
     big, small = (128, 2048, 1024, 4, 32, 32), (20, 1024, 512, 4, 32, 64)
     ws = new_workspace(*[big[i] for i in (0, 2, 1, 3, 4, 5)])
-    assert ws.numel() >= nm.nmspmm_workspace_bytes(*[small[i] for i in (0, 2, 1, 3, 4, 5)])
+    assert ws.numel() >= ws_bytes(*[small[i] for i in (0, 2, 1, 3, 4, 5)])
     for m, k, n, N, M, V in (big, small):
         A, Bp, _ = make_inputs(m, k, n, N, M, V, 21 + m, "int")
         Bc, idx = oracle.compress(Bp, N, M, V)
@@ -709,11 +721,11 @@ def test_gather_kernel_reused_workspace_smaller_shape(monkeypatch):
 def test_gather_kernel_chosen_by_rule():
     """With a workspace, the 64- and 128-row products of the benchmark take
     the direct-gather kernel; 16 rows, V = 16 and tall products do not."""
-    assert nm.nmspmm_kernel_name_ws(64, 8192, 8192, 4, 32, 64).startswith("nm_gather_kernel<r64,c32,")
-    assert nm.nmspmm_kernel_name_ws(128, 8192, 8192, 4, 32, 64).startswith("nm_gather_kernel<r128,c32,")
-    assert not nm.nmspmm_kernel_name_ws(16, 8192, 8192, 4, 32, 64).startswith("nm_gather")
-    assert not nm.nmspmm_kernel_name_ws(64, 2048, 2048, 4, 32, 16).startswith("nm_gather")
-    assert not nm.nmspmm_kernel_name_ws(4096, 4096, 4096, 16, 32, 32).startswith("nm_gather")
+    assert kname_ws(64, 8192, 8192, 4, 32, 64).startswith("nm_gather_kernel<r64,c32,")
+    assert kname_ws(128, 8192, 8192, 4, 32, 64).startswith("nm_gather_kernel<r128,c32,")
+    assert not kname_ws(16, 8192, 8192, 4, 32, 64).startswith("nm_gather")
+    assert not kname_ws(64, 2048, 2048, 4, 32, 16).startswith("nm_gather")
+    assert not kname_ws(4096, 4096, 4096, 16, 32, 32).startswith("nm_gather")
 
 
 # ---- device packer (nmspmm_compress_device) ----

@@ -75,6 +75,27 @@ def test_identity_returns_pruned_B(N, M, V):
     assert np.array_equal(C, Bp.astype(np.float64))
 
 
+@pytest.mark.parametrize("N,M,n", [(2, 4, 12), (3, 8, 7), (4, 32, 64), (16, 32, 40)])
+def test_one_block_is_column_gather_then_dense_gemm(N, M, n):
+    """V = n (one column block, Sec. II-A): every column of C uses the same
+    kept k-rows, so C is A restricted to the kept columns times B restricted
+    to the kept rows.  The kept set comes from the generator's mask, not from
+    idx, and the product is a library GEMM (its own order, so to fp64
+    rounding) and a sequential-k dense sum (bit for bit)."""
+    m, k = 5, 4 * M
+    A, Bp, mask = make_inputs(m, k, n, N, M, n, seed=31 + N + M, dist="normal")
+    kept = np.nonzero(mask[:, 0])[0]
+    assert len(kept) == (k // M) * N and np.all(mask == mask[:, :1])
+    Bc, idx = oracle.compress(Bp, N, M, n)
+    assert np.array_equal(Bc, Bp[kept])                  # compressed rows = kept rows, in k order
+    C = oracle.spmm(A, Bc, idx, m, n, k, N, M, n)
+    Ag = np.ascontiguousarray(A[:, kept])
+    assert np.array_equal(C, dense_sequential(Ag, Bp[kept]))
+    ref = Ag.astype(np.float64) @ Bp[kept].astype(np.float64)
+    scale = np.abs(Ag.astype(np.float64)) @ np.abs(Bp[kept].astype(np.float64))
+    assert np.all(np.abs(C - ref) <= 1e-14 * scale)
+
+
 @pytest.mark.parametrize("N,M,V,k,n", [(2, 4, 4, 48, 16), (3, 8, 2, 48, 6), (1, 4, 1, 52, 5),
                                        (4, 16, 8, 48, 24)])
 def test_bitmask_encoding(N, M, V, k, n):
