@@ -218,11 +218,14 @@ def time_graph(torch, launch, copies, batches, reps):
     return out
 
 
-def cpu_baseline(run, A, Bp, target_s):
-    """The fp64 CPU oracle on the same workload, timed on the host cores."""
+def cpu_baseline(run, A, Bp, target_s, threads=None):
+    """The fp64 CPU oracle on the same workload, timed on the host cores
+    (`threads` OpenMP threads; default: all)."""
     import oracle
     Bc, idx = oracle.compress(Bp, run.N, run.M, run.V)
-    threads = oracle.max_threads()
+    all_threads = oracle.max_threads()
+    threads = threads or all_threads
+    oracle.set_threads(threads)
     # calibrate on a few rows, then pick a row sample worth about target_s
     rows = min(run.m, 16)
     t = time.perf_counter()
@@ -236,12 +239,59 @@ def cpu_baseline(run, A, Bp, target_s):
         t = time.perf_counter()
         oracle.spmm(As, Bc, idx, rows, run.n, run.k, run.N, run.M, run.V)
         times.append(time.perf_counter() - t)
+    oracle.set_threads(all_threads)
     dt = statistics.median(times)
     flops = 2.0 * rows * run.n * run.w
     return {
         "value": flops / dt / 1e12, "unit": "TFLOPS", "cores": threads, "kind": "oracle",
         "sample": (f"{run.name}: {rows} of {run.m} rows of A (full k, n), fp64 oracle, "
                    f"median of {reps} run(s), {dt:.2f} s each"),
+    }
+
+
+def measured_roofs(torch):
+    """The two roofs as this GPU reaches them, from bench/micro's kernels: a
+    streaming read of 4 GiB (well past the 256 MB Infinity Cache) and an
+    fp32 MFMA loop of independent v_mfma_f32_32x32x2_f32 chains.  Best of
+    several launch shapes, median of the timed launches of each."""
+    path = os.path.join(ROOT, "bench", "micro", "libnm_micro.so")
+    if not os.path.exists(path):
+        raise ImportError(f"{path} is not built: run `python bench/micro/build.py`")
+    L = ctypes.CDLL(path)
+    L.nm_micro_hbm_read.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p]
+    L.nm_micro_mfma_f32.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_int, ctypes.c_void_p]
+    L.nm_micro_mfma_f32_flops.argtypes = [ctypes.c_int, ctypes.c_int]
+    L.nm_micro_mfma_f32_flops.restype = ctypes.c_double
+    h = torch.cuda.current_stream().cuda_stream
+    nbytes = 4 << 30
+    buf = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
+    hbm = {}
+    for blocks in (1024, 2048, 4096, 8192):
+        sink = torch.empty(blocks * 256, dtype=torch.int32, device="cuda")
+
+        def rd(i, blocks=blocks, sink=sink):
+            if L.nm_micro_hbm_read(buf.data_ptr(), nbytes, sink.data_ptr(), blocks, h) != 0:
+                raise RuntimeError("nm_micro_hbm_read failed")
+        _, per = time_launches(torch, rd, 10, 2, 0.1)
+        hbm[blocks] = nbytes / (statistics.median(per) * 1e-3) / 1e9
+    del buf
+    mfma = {}
+    iters = 2048
+    for blocks in (256, 512, 1024, 2048):
+        sink = torch.empty(blocks * 256, dtype=torch.float32, device="cuda")
+
+        def mm(i, blocks=blocks, sink=sink):
+            if L.nm_micro_mfma_f32(sink.data_ptr(), iters, blocks, h) != 0:
+                raise RuntimeError("nm_micro_mfma_f32 failed")
+        _, per = time_launches(torch, mm, 10, 2, 0.1)
+        mfma[blocks] = L.nm_micro_mfma_f32_flops(iters, blocks) / (statistics.median(per) * 1e-3) / 1e12
+    torch.cuda.empty_cache()
+    best_hbm, best_mfma = max(hbm, key=hbm.get), max(mfma, key=mfma.get)
+    return {
+        "hbm_read_gbs": round(hbm[best_hbm], 1), "hbm_read_blocks": best_hbm,
+        "mfma_f32_tflops": round(mfma[best_mfma], 2), "mfma_f32_blocks": best_mfma,
+        "spec_hbm_gbs": PEAK_HBM_GBS, "spec_fp32_tflops": PEAK_FP32_TFLOPS,
+        "source": "bench/micro/nm_micro.hip (4 GiB streaming read; 8 chains of v_mfma_f32_32x32x2_f32 per wave)",
     }
 
 
@@ -330,6 +380,21 @@ def measure_extras(torch, nm):
     return out
 
 
+def summary_row(res, roofs):
+    """One workload's compact record: kernel, time, effective rate, fraction
+    of its roof (spec and, where measured, the measured roof), speedup over
+    the dense fp32 GEMM and the ideal M/N."""
+    run = RUNS[res["workload"]]
+    frac_meas = None
+    if roofs:
+        ai = run.useful_flops / run.alg_bytes
+        roof = min(roofs["mfma_f32_tflops"], ai * roofs["hbm_read_gbs"] / 1e3)
+        frac_meas = round(res["eff_tflops"] / roof, 3)
+    return [run.name, res["kernel"], round(res["kernel_ms_median"] * 1e3, 2), round(res["eff_tflops"], 1),
+            round(res["roof_frac"], 3), res["bound"], frac_meas, round(res.get("speedup_vs_dense", 0.0), 2),
+            run.M / run.N]
+
+
 def device_clocks():
     """Current clocks as rocm-smi reports them (None where it is unavailable)."""
     import subprocess
@@ -353,6 +418,7 @@ def main():
     ap.add_argument("--no-table", action="store_true",
                     help="skip the shape x sparsity sweep (matrix-size table A-F x 0-87.5 %%)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--no-roofs", action="store_true", help="skip the roof micro-benchmarks")
     ap.add_argument("--launches-only", type=int, default=0, metavar="L",
                     help="run L untimed launches of the workload and exit (for counter passes)")
     ap.add_argument("--copy-only", type=int, default=0, metavar="L",
@@ -413,6 +479,15 @@ def main():
         log("[bench] cpu baseline (oracle)")
         cpu = cpu_baseline(run, w.host_A, w.host_Bp, args.cpu_seconds)
         log(f"[bench] cpu {json.dumps(cpu)}")
+        one = cpu_baseline(run, w.host_A, w.host_Bp, args.cpu_seconds, threads=1)
+        log(f"[bench] cpu 1 thread {json.dumps(one)}")
+        cpu["one_thread"] = {"value": one["value"], "cores": 1, "sample": one["sample"]}
+
+    roofs = None
+    if not args.no_roofs:
+        log("[bench] measured roofs (bench/micro)")
+        roofs = measured_roofs(torch)
+        log(f"[bench] roofs {json.dumps(roofs)}")
 
     sweep = []
     if not args.no_sweep:
@@ -480,11 +555,16 @@ def main():
         "paper_context": {"hardware": "NVIDIA A100 80GB PCIe (clock locked, 14.7 TFLOPS fp32 peak)",
                           "workload": "m=n=k=4096, vector length not stated",
                           "pct_of_fp32_peak_50_62.5_75_87.5": [96, 93, 95, 88]},
-        "sweep": sweep,
         "shape_sparsity_table": table,
+        "sweep": sweep,
         **extras,
         "device": torch.cuda.get_device_name(0),
         "device_clocks": device_clocks(),
+        "measured_roofs": roofs,
+        # last, so that a reader of the line's tail sees every workload
+        "summary_cols": ["run", "kernel", "us", "eff_tflops", "roof_frac", "bound", "roof_frac_measured",
+                         "x_dense_fp32", "ideal_M_over_N"],
+        "summary": [summary_row(r, roofs) for r in [head] + sweep],
     }
     print(json.dumps(line), flush=True)
 

@@ -30,6 +30,22 @@ def test_library_exports_every_declared_symbol():
         assert ctypes.cast(getattr(L, name), ctypes.c_void_p).value
 
 
+def test_micro_library_exports_every_declared_symbol():
+    """The roof micro-benchmarks' library (bench/micro) exports what
+    include/nm_micro.h declares."""
+    text = open(os.path.join(ROOT, "include", "nm_micro.h")).read()
+    names = sorted(set(re.findall(r"NM_MICRO_API\s+[\w\s\*]*?\b(nm_micro_\w+)\s*\(", text)))
+    assert names == ["nm_micro_hbm_read", "nm_micro_mfma_f32", "nm_micro_mfma_f32_flops"]
+    L = ctypes.CDLL(os.path.join(ROOT, "bench", "micro", "libnm_micro.so"))
+    for name in names:
+        assert ctypes.cast(getattr(L, name), ctypes.c_void_p).value, name
+    L.nm_micro_mfma_f32_flops.argtypes = [ctypes.c_int, ctypes.c_int]
+    L.nm_micro_mfma_f32_flops.restype = ctypes.c_double
+    assert L.nm_micro_mfma_f32_flops(10, 3) == 2 * 32 * 32 * 2 * 8 * 10 * 4 * 3
+    L.nm_micro_hbm_read.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p]
+    assert L.nm_micro_hbm_read(0x1000, 100, 0x1000, 8, None) == 1        # not a multiple of 16: refused
+
+
 def test_default_dispatch_reads_no_environment(monkeypatch):
     """The default entry points ignore tuning-looking environment variables;
     overrides reach the library only through the *_tuned calls."""
