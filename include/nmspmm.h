@@ -17,8 +17,9 @@
  * with no M/N rescaling (a caller wanting Eq. 1's factor scales Bc).
  *
  * Every entry point is extern "C", returns a status code and never throws.
- * The library holds no global state and is safe to call from several host
- * threads.
+ * The library holds no global state (beyond the static scratch array of
+ * nmspmm_run_noalloc and its per-device address) and is safe to call from
+ * several host threads.
  */
 #ifndef NMSPMM_H
 #define NMSPMM_H
@@ -47,8 +48,16 @@ typedef enum {
      * products overflow int64) */
     NMSPMM_ERR_UNSUPPORTED = 2,
     /* the HIP runtime reported an error while launching */
-    NMSPMM_ERR_HIP = 3
+    NMSPMM_ERR_HIP = 3,
+    /* nmspmm_run_noalloc only: the shape's kernels need more scratch than
+     * its static array holds (NMSPMM_NOALLOC_SCRATCH_BYTES); nothing ran */
+    NMSPMM_ERR_SCRATCH = 4
 } nmspmm_status_t;
+
+/* Size of the static device scratch array of nmspmm_run_noalloc: 16 MiB per
+ * device, enough for the direct-gather kernel's transposed A and offsets up
+ * to 128 rows at k = n = 16384 (4:32, V = 64). */
+#define NMSPMM_NOALLOC_SCRATCH_BYTES (16u << 20)
 
 /* Number of fp32 elements of Bc, (k/M)*N*n, or -1 if (k, n, N, M) is invalid
  * (Sec. II-A: w = k*N/M rows). */
@@ -192,6 +201,28 @@ NMSPMM_API const char *nmspmm_kernel_name(int64_t m, int64_t n, int64_t k, int N
  * bytes ("+prep": the transposition kernel runs first; "+ws": partial tiles
  * go through the workspace). */
 NMSPMM_API const char *nmspmm_kernel_name_ws(int64_t m, int64_t n, int64_t k, int N, int M, int V);
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc):
+ * nmspmm_run_ws with its workspace in a static device array of
+ * NMSPMM_NOALLOC_SCRATCH_BYTES instead of caller memory.  Same product (Eq. 1
+ * as read above), same epilogue, same kernels and bit-identical results as
+ * nmspmm_run_ws given a workspace of nmspmm_workspace_bytes.  The call
+ * allocates nothing and calls no allocating routine; every device the
+ * library runs on holds its own copy of the array from the library's load
+ * until the process ends.  The array's device address is looked up on the
+ * first call on each device (make that first call outside graph capture).
+ * Every call on a device shares that device's array: calls that overlap on
+ * one device (several streams or host threads) race and must be serialised
+ * by the caller.  Each call rewrites every scratch byte its kernels read, so
+ * the array's old contents never matter.  Errors: as nmspmm_run_ex, plus
+ * NMSPMM_ERR_SCRATCH when nmspmm_workspace_bytes for the shape exceeds
+ * NMSPMM_NOALLOC_SCRATCH_BYTES (checked before anything is launched) and
+ * NMSPMM_ERR_HIP when the array's address cannot be obtained. */
+NMSPMM_API nmspmm_status_t nmspmm_run_noalloc(const float *A, const float *Bc, const uint8_t *idx,
+                                   float *C, int64_t m, int64_t n, int64_t k, int N,
+                                   int M, int V, float alpha, const float *bias,
+                                   nmspmm_act_t act, hipStream_t stream);
 
 /* ---- Tuning entry points: for tile sweeps and forced-variant tests only ----
  * The same product, Eq. 1 as read above, with the kernel choice overridden.

@@ -18,6 +18,8 @@ NMSPMM_OK = 0
 NMSPMM_ERR_INVALID_ARG = 1
 NMSPMM_ERR_UNSUPPORTED = 2
 NMSPMM_ERR_HIP = 3
+NMSPMM_ERR_SCRATCH = 4
+NMSPMM_NOALLOC_SCRATCH_BYTES = 16 << 20
 
 NMSPMM_ACT_NONE = 0
 NMSPMM_ACT_RELU = 1
@@ -28,7 +30,7 @@ EXPORTS = (
     "nmspmm_bc_elems", "nmspmm_idx_bytes", "nmspmm_compress", "nmspmm_compress_device",
     "nmspmm_run", "nmspmm_run_ex", "nmspmm_run_ws", "nmspmm_workspace_bytes", "nmspmm_validate_idx",
     "nmspmm_status_string", "nmspmm_kernel_name", "nmspmm_kernel_name_ws",
-    "nmspmm_run_tuned", "nmspmm_kernel_name_tuned", "nmspmm_workspace_bytes_tuned",
+    "nmspmm_run_tuned", "nmspmm_kernel_name_tuned", "nmspmm_workspace_bytes_tuned", "nmspmm_run_noalloc",
 )
 
 
@@ -85,6 +87,8 @@ def lib():
     L.nmspmm_kernel_name_tuned.restype = ctypes.c_char_p
     L.nmspmm_workspace_bytes_tuned.argtypes = [I64, I64, I64, I, I, I, ctypes.c_char_p]
     L.nmspmm_workspace_bytes_tuned.restype = I64
+    L.nmspmm_run_noalloc.argtypes = [P, P, P, P, I64, I64, I64, I, I, I, ctypes.c_float, P, I, P]
+    L.nmspmm_run_noalloc.restype = I
     _lib = L
     return L
 
@@ -196,6 +200,16 @@ def nmspmm_run_ws(A, Bc, idx, C, m: int, n: int, k: int, N: int, M: int, V: int,
                          _name="nmspmm_run_ws", _workspace=workspace)
 
 
+def nmspmm_run_noalloc(A, Bc, idx, C, m: int, n: int, k: int, N: int, M: int, V: int,
+                       alpha: float = 1.0, bias=None, act: str = "none", stream=None):
+    """nmspmm_run_ws with the library's static per-device scratch array as the
+    workspace (for callers that cannot allocate); raises NmSpmmError with
+    NMSPMM_ERR_SCRATCH when the shape needs more than
+    NMSPMM_NOALLOC_SCRATCH_BYTES.  Calls that overlap on one device race."""
+    return nmspmm_run_ex(A, Bc, idx, C, m, n, k, N, M, V, alpha, bias, act, stream,
+                         _name="nmspmm_run_noalloc")
+
+
 def nmspmm_run_ex(A, Bc, idx, C, m: int, n: int, k: int, N: int, M: int, V: int,
                   alpha: float = 1.0, bias=None, act: str = "none", stream=None, tuning=None,
                   _name: str = "nmspmm_run_ex", _workspace=None):
@@ -226,6 +240,10 @@ def nmspmm_run_ex(A, Bc, idx, C, m: int, n: int, k: int, N: int, M: int, V: int,
                                     0 if _workspace is None else _workspace.numel(),
                                     tuning_string(tuning), stream.cuda_stream)
             _name = "nmspmm_run_tuned"
+        elif _name == "nmspmm_run_noalloc":
+            st = L.nmspmm_run_noalloc(A.data_ptr(), Bc.data_ptr(), idx.data_ptr(), C.data_ptr(),
+                                      m, n, k, N, M, V, float(alpha),
+                                      None if bias is None else bias.data_ptr(), ACTS[act], stream.cuda_stream)
         elif _name == "nmspmm_run":
             st = L.nmspmm_run(A.data_ptr(), Bc.data_ptr(), idx.data_ptr(), C.data_ptr(),
                               m, n, k, N, M, V, stream.cuda_stream)

@@ -120,6 +120,9 @@ extern "C" const char *nmspmm_status_string(nmspmm_status_t s)
     case NMSPMM_ERR_INVALID_ARG: return "invalid argument";
     case NMSPMM_ERR_UNSUPPORTED: return "unsupported request";
     case NMSPMM_ERR_HIP: return "HIP runtime error";
+    case NMSPMM_ERR_SCRATCH:
+        return "the shape needs more scratch than nmspmm_run_noalloc's static array holds "
+               "(NMSPMM_NOALLOC_SCRATCH_BYTES); call nmspmm_run_ws with a workspace instead";
     }
     return "unknown status";
 }

@@ -10,10 +10,12 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cstdint>
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 
 #include "nmspmm.h"
 #include "nmspmm_gather.h"
@@ -939,3 +941,60 @@ extern "C" nmspmm_status_t nmspmm_run(const float *A, const float *Bc, const uin
     return nmspmm_run_ex(A, Bc, idx, C, m, n, k, N, M, V, 1.f, nullptr, NMSPMM_ACT_NONE, stream);
 }
 
+// ---------------------------------------------------------------------------
+// nmspmm_run_noalloc: nmspmm_run_ws with the workspace in a static device
+// array instead of caller memory, for callers that cannot allocate.  Every
+// device the library runs on holds its own copy of the array (module scope)
+// until the process ends; its address on a device is looked up once, on the
+// first call there, and the kernels take that address.  Each call rewrites
+// every byte of the scratch that its kernels read (the transposed A and the
+// gather offsets, or every split's partial tiles), so nothing has to start
+// at zero; calls that overlap on one device share the array and race.
+// ---------------------------------------------------------------------------
+namespace {
+
+static __device__ __align__(256) unsigned char scratch[NMSPMM_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::atomic<void *> g_scratch[kMaxDevices];
+std::mutex g_scratch_mu;
+
+// The current device's address of `scratch` (the host-side symbol is only a
+// stand-in for it).
+hipError_t scratch_on_current_device(void **out)
+{
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    void *p = g_scratch[dev].load(std::memory_order_acquire);
+    if (!p) {
+        std::lock_guard<std::mutex> lock(g_scratch_mu);
+        p = g_scratch[dev].load(std::memory_order_relaxed);
+        if (!p) {
+            e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+            if (e != hipSuccess || !p) return e != hipSuccess ? e : hipErrorInvalidSymbol;
+            g_scratch[dev].store(p, std::memory_order_release);
+        }
+    }
+    *out = p;
+    return hipSuccess;
+}
+
+}  // namespace
+
+extern "C" nmspmm_status_t nmspmm_run_noalloc(const float *A, const float *Bc, const uint8_t *idx, float *C,
+                                              int64_t m, int64_t n, int64_t k, int N, int M, int V,
+                                              float alpha, const float *bias, nmspmm_act_t act,
+                                              hipStream_t stream)
+{
+    const nmspmm_status_t st = check_run_args(A, Bc, idx, C, m, n, k, N, M, V, bias, act);
+    if (st != NMSPMM_OK || m == 0 || n == 0) return st;
+    // the workspace the plan of nmspmm_run_ws takes for these buffers
+    const int64_t need = plan_ws_bytes(make_ws_plan(A, Bc, C, m, n, k, N, M, V, kNoTuning));
+    if (need > (int64_t)NMSPMM_NOALLOC_SCRATCH_BYTES) return NMSPMM_ERR_SCRATCH;
+    void *ws = nullptr;
+    if (need > 0 && scratch_on_current_device(&ws) != hipSuccess) return NMSPMM_ERR_HIP;
+    return run_impl(A, Bc, idx, C, m, n, k, N, M, V, alpha, bias, act, ws,
+                    need > 0 ? (size_t)NMSPMM_NOALLOC_SCRATCH_BYTES : 0, kNoTuning, stream);
+}

@@ -22,7 +22,7 @@ def declared_symbols():
 
 def test_library_exports_every_declared_symbol():
     names = declared_symbols()
-    assert len(names) == 15
+    assert len(names) == 16
     assert sorted(nm.EXPORTS) == names
     L = nm.lib()
     for name in names:
@@ -69,6 +69,21 @@ def test_tuning_string_is_checked():
                                   None, 0, bad, None) == nm.NMSPMM_ERR_INVALID_ARG, bad
     assert L.nmspmm_kernel_name_tuned(*shape, 0, b"") == nm.nmspmm_kernel_name(*shape).encode()
     assert L.nmspmm_kernel_name_tuned(*shape, 0, None) == nm.nmspmm_kernel_name(*shape).encode()
+
+
+def test_noalloc_rejects_shapes_beyond_its_scratch_before_any_gpu_call():
+    """nmspmm_run_noalloc checks the shape's workspace against its static
+    array before touching the GPU: 128 rows at k = 65536 need a 32 MiB
+    transposed A, more than the array's 16 MiB."""
+    L = nm.lib()
+    assert nm.nmspmm_workspace_bytes(128, 8192, 65536, 4, 32, 64) > nm.NMSPMM_NOALLOC_SCRATCH_BYTES
+    st = L.nmspmm_run_noalloc(256, 256, 256, 256, 128, 8192, 65536, 4, 32, 64, ctypes.c_float(1.0), None, 0, None)
+    assert st == nm.NMSPMM_ERR_SCRATCH
+    assert "scratch" in nm.nmspmm_status_string(st)
+    # argument errors come first, and empty products launch nothing
+    assert L.nmspmm_run_noalloc(0, 0, 0, 0, 8, 64, 65, 4, 32, 32, ctypes.c_float(1.0), None, 0, None) == \
+        nm.NMSPMM_ERR_INVALID_ARG
+    assert L.nmspmm_run_noalloc(0, 0, 0, 0, 0, 64, 64, 4, 32, 32, ctypes.c_float(1.0), None, 0, None) == nm.NMSPMM_OK
 
 
 def test_size_helpers():
