@@ -384,7 +384,7 @@ def summary_row(res, roofs):
     """One workload's compact record: kernel, time, effective rate, fraction
     of its roof (spec and, where measured, the measured roof), speedup over
     the dense fp32 GEMM and the ideal M/N."""
-    run = RUNS[res["workload"]]
+    run = RUNS.get(res["workload"]) or table_runs()[res["workload"]]
     frac_meas = None
     if roofs:
         ai = run.useful_flops / run.alg_bytes
@@ -412,7 +412,9 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=100)
-    ap.add_argument("--workload", default="R2", choices=sorted(RUNS))
+    ap.add_argument("--workload", default="R2", choices=sorted(RUNS) + sorted(table_runs()),
+                    help="the headline run (default R2), another benchmark run, or a point of the shape x "
+                         "sparsity sweep (A-32 .. F-4), e.g. for counter passes with --launches-only")
     ap.add_argument("--no-sweep", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-table", action="store_true",
@@ -439,7 +441,7 @@ def main():
     torch.set_float32_matmul_precision("highest")
     assert torch.cuda.is_available(), "bench.py needs a GPU"
 
-    run = RUNS[args.workload]
+    run = RUNS.get(args.workload) or table_runs()[args.workload]
     if args.copy_only:
         src = torch.empty(1 << 28, dtype=torch.float32, device="cuda").fill_(1.0)
         dst = torch.empty_like(src)
