@@ -48,12 +48,19 @@ def lib():
     binds to the HIP runtime torch already loaded (same soname), keeping
     torch's streams and allocations valid inside the library."""
     global _lib
-    if _lib is not None:
-        return _lib
+    if _lib is None:
+        _lib = load(LIB_PATH)
+    return _lib
+
+
+def load(path: str):
+    """A ctypes handle on a build of the library at `path` (the product
+    library, or its NaN-poisoned debug twin for the LDS race tests), with
+    every entry point's signature declared."""
     import torch  # noqa: F401  (loads torch's libamdhip64 before ours)
-    if not os.path.exists(LIB_PATH):
-        raise ImportError(f"{LIB_PATH} is not built: run `python -m paper_2503_01253_amd.build`")
-    L = ctypes.CDLL(LIB_PATH)
+    if not os.path.exists(path):
+        raise ImportError(f"{path} is not built: run `python -m paper_2503_01253_amd.build`")
+    L = ctypes.CDLL(path)
     I64, I, P = ctypes.c_int64, ctypes.c_int, ctypes.c_void_p
     L.nmspmm_bc_elems.argtypes = [I64, I64, I, I]
     L.nmspmm_bc_elems.restype = I64
@@ -89,7 +96,6 @@ def lib():
     L.nmspmm_workspace_bytes_tuned.restype = I64
     L.nmspmm_run_noalloc.argtypes = [P, P, P, P, I64, I64, I64, I, I, I, ctypes.c_float, P, I, P]
     L.nmspmm_run_noalloc.restype = I
-    _lib = L
     return L
 
 

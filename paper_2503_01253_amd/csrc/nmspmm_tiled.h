@@ -199,14 +199,35 @@ constexpr uint32_t OOB = 0x80000000u;  // an offset past every buffer used here
 __device__ __forceinline__ int64_t min64(int64_t a, int64_t b) { return a < b ? a : b; }
 __device__ __forceinline__ int64_t max64(int64_t a, int64_t b) { return a > b ? a : b; }
 
+// Debug build switch (off in the product library): with NMSPMM_POISON_LDS=1
+// every buffer->LDS DMA first fills its own destination with NaN (offset
+// bytes: a NaN bit pattern, which the readers clamp to the last offset of
+// the window, a wrong but in-bounds column), waits for those stores, then
+// issues the DMA; the tiled kernel also fills each A_s slot with NaN as soon
+// as it is free.  A reader that runs ahead of a missing wait or barrier then
+// reads NaN or a wrong column instead of stale data that may happen to be
+// right, and the exact-result tests fail.
+#ifndef NMSPMM_POISON_LDS
+#define NMSPMM_POISON_LDS 0
+#endif
+
 // One buffer->LDS DMA instruction: lane l's W bytes from byte offset `off`
-// of the buffer land at dst + l*W.  (The width is spelled as a literal in
-// each branch: the builtin needs an integer constant that is not
-// template-dependent.)
+// of the buffer land at dst + l*W (W = 1: a zero-extended dword at dst +
+// l*4).  (The width is spelled as a literal in each branch: the builtin needs
+// an integer constant that is not template-dependent.)
 template <int W>
 __device__ __forceinline__ void lds_dma(__amdgpu_buffer_rsrc_t rsrc, void *dst, uint32_t off)
 {
     static_assert(W == 1 || W == 4 || W == 16, "DMA width");
+    if constexpr (NMSPMM_POISON_LDS) {
+        const int l = (int)__builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
+        const float nan = __builtin_nanf("");
+        if constexpr (W == 16)
+            *reinterpret_cast<f32x4 *>(static_cast<unsigned char *>(dst) + 16 * l) = f32x4{nan, nan, nan, nan};
+        else
+            *reinterpret_cast<float *>(static_cast<unsigned char *>(dst) + 4 * l) = nan;
+        __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (0 << 8) | (3 << 14));  // lgkmcnt(0)
+    }
     if constexpr (W == 16)
         __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void *)dst, 16, (int)off, 0, 0, 0);
     else if constexpr (W == 4)
@@ -448,6 +469,16 @@ __global__ __launch_bounds__(T::NT) void nm_tiled_kernel(TiledArgs p)
     for (int it = 0; it < nst; ++it) {
         const int cur = it & 1;
         const bool next = it + 1 < nst;
+        if constexpr (NMSPMM_POISON_LDS && S::TWO_A) {
+            // the other A_s slot is free (every wave passed the barrier after
+            // its last read): NaN in the places this wave's store will fill
+            const float nan = __builtin_nanf("");
+#pragma unroll
+            for (int ch = 0; ch < ACH; ++ch)
+#pragma unroll
+                for (int t = 0; t < 4; ++t) ra[ch][t] = f32x4{nan, nan, nan, nan};
+            store_a(cur ^ 1);
+        }
         prep_offsets(cur);
         fetch(cur, 0, 0);
 #pragma unroll
