@@ -275,13 +275,17 @@ int preferences(int64_t m, int64_t n, int N, int M, int V, const TileInfo **out)
 
 // The streaming kernel re-reads Bc once per 16 rows of C (mostly from L2 and
 // the Infinity Cache), the tiled kernel once per 128 or more.  On MI355X the
-// streaming kernel is faster up to 128 rows at k = n = 8192, and on small
-// products (m * w below 2^19, e.g. 512 x 2048 x 2048 at 62.5 %), where the
-// tiled kernel's grid would be mostly split-k.
+// streaming kernel is faster up to 128 rows at k = n = 8192, and on products
+// up to 1024 rows with m * w at most 2^20, where the tiled kernel's grid would
+// be mostly split-k.  Measured (graph replay, per call) against the tiled
+// kernel with split-k: 512 x 1024 x 1024 at N = M 40.7 -> 21.2 us, 512 x 2048
+// x 2048 at N = M 66.6 -> 57.2 and at 16:32 50.3 -> 35.1, 1024 x 2048 x 2048
+// at 16:32 69.3 -> 64.0, 12:32 63.0 -> 52.8, 8:32 52.3 -> 43.4; at N = M
+// (m * w = 2^21) the tiled kernel stays ahead (101.0 against 103.2).
 bool prefer_streaming(int64_t m, int64_t k, int N, int M)
 {
     const int64_t w = (k / M) * N;
-    return m <= 128 || (m <= 1024 && m * w < (int64_t(1) << 19));
+    return m <= 128 || (m <= 1024 && m * w <= (int64_t(1) << 20));
 }
 
 // Overrides of the dispatch rules, for tuning sweeps and the forced-variant
@@ -372,9 +376,14 @@ bool plan_skinny(const float *A, const float *Bc, const float *C, int64_t m, int
     if (tiles_m * tiles_n > (1 << 24)) return false;
     const int64_t G = k / M, ntiles = tiles_m * tiles_n;
     // about one workgroup per CU, but at least 32 compressed rows (one quad
-    // per wave) per workgroup
+    // per wave) per workgroup; none when a workgroup's whole product is under
+    // 2^21 flops, where the zero fill and the atomics cost more than the
+    // fuller grid gives (graph replay: 512 x 512 x 512 at 16:32 10.8 ->
+    // 10.3 us, at 8:32 9.7 -> 8.6, 256 x 256 x 256 at 16:32 8.9 -> 8.4; at
+    // N = M, 2^21 flops per workgroup, split 2 stays ahead, 12.6 against 13.7)
     int64_t splits = std::min<int64_t>((256 + ntiles - 1) / ntiles, G * N / 32);
     splits = std::max<int64_t>(1, std::min<int64_t>(splits, 64));
+    if (2 * skinny_rows(rt) * (int64_t)cols * (G * N) < (int64_t(1) << 21)) splits = 1;
     const int fs = t.splits;
     if (fs >= 1) splits = std::min<int64_t>(fs, std::max<int64_t>(G, 1));
     // longer runs per wave when each workgroup walks all of k
