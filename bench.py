@@ -339,8 +339,9 @@ def measure(torch, nm, run, steps, warmup, with_dense, graph=False, warm_seconds
 
 def measure_extras(torch, nm):
     """The steps beside the product: the fused epilogue of nmspmm_run_ex on the
-    MLP-shaped run (alpha = M/N, bias, GELU, against the plain product), and
-    the device packer nmspmm_compress_device on the headline's dense B."""
+    MLP-shaped run (alpha = M/N, bias, GELU, against the plain product), the
+    device packer nmspmm_compress_device on the headline's dense B, and Eq. 2's
+    confusion matrix nmspmm_confusion on the headline's output size."""
     out = {}
     r = RUNS["R4"]
     w = Workload(r, torch, nm, min_copies=2)
@@ -376,6 +377,24 @@ def measure_extras(torch, nm):
     out["device_compress"] = {"workload": f"B of {r.name}: {r.k} x {r.n}, {r.N}:{r.M}, V={r.V}",
                               "ms": ms, "gb_s": moved / (ms * 1e-3) / 1e9}
     del dB, dBc, didx
+    torch.cuda.empty_cache()
+    # Eq. 2's confusion matrix on the headline's m x n output: two reads and
+    # one write of 4 bytes per output, over two sets of arrays (384 MB, past
+    # the Infinity Cache)
+    sets = [[torch.randn(r.m, r.n, device="cuda") for _ in range(3)] for _ in range(2)]
+
+    def cf(i):
+        cs, cd, wt = sets[i % 2]
+        st = L.nmspmm_confusion(cs.data_ptr(), cd.data_ptr(), wt.data_ptr(), r.m, r.n, h)
+        if st != 0:
+            raise RuntimeError(nm.nmspmm_status_string(st))
+    _, per = time_launches(torch, cf, 40, 4, 0.2)
+    ms = statistics.median(per)
+    moved = 12.0 * r.m * r.n
+    out["eq2_confusion"] = {"workload": f"W = |C' - C| / (m*n) on {r.m} x {r.n} fp32 outputs",
+                            "ms": ms, "gb_s": moved / (ms * 1e-3) / 1e9,
+                            "frac_hbm_peak": moved / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS}
+    del sets
     torch.cuda.empty_cache()
     return out
 
@@ -531,7 +550,7 @@ def main():
 
     extras = {}
     if not args.no_sweep:
-        log("[bench] epilogue and device packer")
+        log("[bench] epilogue, device packer and Eq. 2 confusion matrix")
         extras = measure_extras(torch, nm)
         log(f"[bench] extras {json.dumps(extras)}")
 

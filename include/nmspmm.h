@@ -14,7 +14,8 @@
  * offset in [0, M) inside window g.  Offsets of one (g, b) are strictly
  * increasing.  The product computed is Eq. 1 read as
  *   C[i][j] = sum_{u<w} A[i][floor(u/N)*M + idx[u][floor(j/V)]] * Bc[u][j]
- * with no M/N rescaling (a caller wanting Eq. 1's factor scales Bc).
+ * with no M/N rescaling (nmspmm_run_ex with alpha = M/N applies Eq. 1's
+ * factor).
  *
  * Every entry point is extern "C", returns a status code and never throws.
  * The library holds no global state (beyond the static scratch array of
@@ -180,6 +181,24 @@ NMSPMM_API nmspmm_status_t nmspmm_run_ws(const float *A, const float *Bc, const 
 NMSPMM_API nmspmm_status_t nmspmm_compress_device(const float *B_dense, int64_t k, int64_t n,
                                        int N, int M, int V, float *Bc, uint8_t *idx,
                                        hipStream_t stream);
+
+/* Eq. 2 (Sec. II-A), the confusion matrix between the N:M output and the
+ * dense output of the same A:
+ *   W[i][j] = |C_sparse[i][j] - C_dense[i][j]| / (m*n)
+ * where C_sparse is Eq. 1's output with its M/N factor (nmspmm_run_ex with
+ * alpha = M/N) and C_dense the product of A with the unpruned B (for
+ * instance nmspmm_run on the N = M compression of B, which keeps every row).
+ * DEVICE pointers, all on the current HIP device, m x n fp32 row-major.  W is
+ * overwritten and may be the same array as C_sparse or C_dense (in place);
+ * any other overlap is not allowed.  Each W[i][j] is the fp64 quotient of
+ * the fp64 difference by the fp64 value of m*n, rounded once to fp32 (the
+ * fp32 inputs convert to fp64 exactly).  Asynchronous on `stream`, allocates
+ * nothing; m == 0 or n == 0 returns NMSPMM_OK without a launch.  Errors:
+ * NMSPMM_ERR_INVALID_ARG (negative size, null pointer with non-empty data),
+ * NMSPMM_ERR_UNSUPPORTED (a pointer not aligned to 4 bytes, m*n beyond
+ * int64), NMSPMM_ERR_HIP (the launch failed). */
+NMSPMM_API nmspmm_status_t nmspmm_confusion(const float *C_sparse, const float *C_dense, float *W,
+                                 int64_t m, int64_t n, hipStream_t stream);
 
 /* Host check of the pattern rules (Sec. II-A): every (group, block) has N
  * offsets, each < M, strictly increasing.  HOST pointer, O(w*q).

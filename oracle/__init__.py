@@ -16,7 +16,7 @@ from .build import LIB_PATH, build
 
 __all__ = [
     "build", "lib", "spmm", "bound", "compress", "decompress", "validate", "epilogue",
-    "set_threads", "max_threads", "check", "CheckResult", "PARITY_RTOL",
+    "dense", "confusion", "set_threads", "max_threads", "check", "CheckResult", "PARITY_RTOL",
 ]
 
 # Parity bar: |C_gpu - C_ref| <= PARITY_RTOL * sum_k |A_ik| |B_kj| for every
@@ -47,6 +47,10 @@ def lib():
         L.oracle_set_threads.argtypes = [_I]
         L.oracle_epilogue.argtypes = [_D, _I64, _I64, ctypes.c_double, _F, _I]
         L.oracle_epilogue.restype = _I
+        L.oracle_dense.argtypes = [_F, _F, _D, _I64, _I64, _I64]
+        L.oracle_dense.restype = _I
+        L.oracle_confusion.argtypes = [_D, _D, _D, _I64, _I64]
+        L.oracle_confusion.restype = _I
         for f in (L.oracle_spmm, L.oracle_bound, L.oracle_compress, L.oracle_decompress,
                   L.oracle_validate, L.oracle_shape_ok, L.oracle_max_threads):
             f.restype = _I
@@ -132,6 +136,33 @@ def epilogue(C, alpha=1.0, bias=None, act="none"):
     if st != 0:
         raise ValueError(f"oracle_epilogue failed ({st})")
     return out
+
+
+def dense(A, B):
+    """C = A * B with the unpruned B (the dense output of Eq. 2), fp64."""
+    A, B = _f32(A), _f32(B)
+    m, k = A.shape
+    k2, n = B.shape
+    if k2 != k:
+        raise ValueError(f"inner sizes differ: {k} and {k2}")
+    C = np.empty((m, n), dtype=np.float64)
+    if lib().oracle_dense(_p(A, _F), _p(B, _F), _p(C, _D), m, n, k):
+        raise ValueError("oracle_dense: bad shape")
+    return C
+
+
+def confusion(Cs, C):
+    """Eq. 2: W = |Cs - C| / (m*n) in fp64, Cs the N:M output with Eq. 1's
+    M/N factor and C the dense output."""
+    Cs = np.ascontiguousarray(Cs, dtype=np.float64)
+    C = np.ascontiguousarray(C, dtype=np.float64)
+    if Cs.shape != C.shape or Cs.ndim != 2:
+        raise ValueError(f"shape mismatch {Cs.shape} {C.shape}")
+    m, n = C.shape
+    W = np.empty((m, n), dtype=np.float64)
+    if lib().oracle_confusion(_p(Cs, _D), _p(C, _D), _p(W, _D), m, n):
+        raise ValueError("oracle_confusion: bad shape")
+    return W
 
 
 def set_threads(t: int) -> None:

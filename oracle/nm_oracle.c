@@ -31,6 +31,8 @@
  *    accumulate plain products (the inner kernel of Sec. III-B), and the
  *    operator C = A (*) (B, D) is the product with the pruned B.
  *  - Offsets within one (group, block) are stored strictly increasing.
+ *  - Eq. 2's C is the product with the unpruned B and its C' is Eq. 1's
+ *    output with the factor M/N; W divides by m*n as printed.
  *  - The paper leaves the pruning rule to pruning algorithms (Sec. II-B); the
  *    compressor keeps the N rows of largest squared L2 norm over the block's
  *    V columns, ties going to the smaller offset.  On an already pruned
@@ -46,6 +48,10 @@
  *  - oracle_compress recovers the generator's mask and round-trips through
  *    oracle_decompress; oracle_bound equals |A| * |B_pruned| from a library
  *    matmul to fp64 rounding.
+ *  - oracle_dense equals oracle_spmm bit for bit at N == M (every row kept,
+ *    same order) and a library matmul to fp64 rounding.
+ *  - oracle_confusion reproduces a hand-worked case, the closed form
+ *    (M/N - 1) * |A * B| / (m*n) on an already pruned B, and zero at N == M.
  */
 #include <math.h>
 #include <stdint.h>
@@ -242,5 +248,41 @@ int oracle_epilogue(double *C, int64_t m, int64_t n, double alpha, const float *
             C[i * n + j] = y;
         }
     }
+    return 0;
+}
+
+/* The dense product that Eq. 2 compares against (Sec. II-A): A (m x k) times
+ * the unpruned B (k x n),
+ *   C[i][j] = sum_{kk=0}^{k-1} A[i][kk] * B[kk][j]
+ * accumulated in fp64 with kk increasing for every (i, j).  Returns 1 for a
+ * negative size. */
+int oracle_dense(const float *A, const float *B, double *C, int64_t m, int64_t n, int64_t k)
+{
+    if (m < 0 || n < 0 || k < 0) return 1;
+#pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < m; ++i) {
+        double *c = C + i * n;
+        const float *a = A + i * k;
+        for (int64_t j = 0; j < n; ++j) c[j] = 0.0;
+        for (int64_t kk = 0; kk < k; ++kk) {
+            const double av = (double)a[kk];
+            const float *brow = B + kk * n;
+            for (int64_t j = 0; j < n; ++j) c[j] += av * (double)brow[j];
+        }
+    }
+    return 0;
+}
+
+/* Eq. 2 (Sec. II-A), the confusion matrix between the N:M output Cs (Eq. 1
+ * with its M/N factor, i.e. oracle_spmm followed by oracle_epilogue with
+ * alpha = M/N) and the dense output C (oracle_dense), both m x n:
+ *   W[i][j] = |Cs[i][j] - C[i][j]| / (m * n)
+ * in fp64, m * n taken as an fp64 value.  Returns 1 for a negative size. */
+int oracle_confusion(const double *Cs, const double *C, double *W, int64_t m, int64_t n)
+{
+    if (m < 0 || n < 0) return 1;
+    const double mn = (double)m * (double)n;
+    for (int64_t i = 0; i < m; ++i)
+        for (int64_t j = 0; j < n; ++j) W[i * n + j] = fabs(Cs[i * n + j] - C[i * n + j]) / mn;
     return 0;
 }

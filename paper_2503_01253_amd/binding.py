@@ -31,6 +31,7 @@ EXPORTS = (
     "nmspmm_run", "nmspmm_run_ex", "nmspmm_run_ws", "nmspmm_workspace_bytes", "nmspmm_validate_idx",
     "nmspmm_status_string", "nmspmm_kernel_name", "nmspmm_kernel_name_ws",
     "nmspmm_run_tuned", "nmspmm_kernel_name_tuned", "nmspmm_workspace_bytes_tuned", "nmspmm_run_noalloc",
+    "nmspmm_confusion",
 )
 
 
@@ -96,6 +97,8 @@ def load(path: str):
     L.nmspmm_workspace_bytes_tuned.restype = I64
     L.nmspmm_run_noalloc.argtypes = [P, P, P, P, I64, I64, I64, I, I, I, ctypes.c_float, P, I, P]
     L.nmspmm_run_noalloc.restype = I
+    L.nmspmm_confusion.argtypes = [P, P, P, I64, I64, P]
+    L.nmspmm_confusion.restype = I
     return L
 
 
@@ -287,3 +290,25 @@ def nmspmm_compress_device(B_dense, Bc, idx, N: int, M: int, V: int, stream=None
                                           idx.data_ptr(), stream.cuda_stream)
     _check("nmspmm_compress_device", st)
     return Bc, idx
+
+
+def nmspmm_confusion(C_sparse, C_dense, W, stream=None):
+    """Eq. 2's confusion matrix W = |C_sparse - C_dense| / (m*n) on the GPU,
+    asynchronously on ``stream`` (default: torch's current stream).
+    C_sparse (Eq. 1's output with its M/N factor, e.g. from nmspmm_run_ex with
+    alpha = M/N), C_dense (the product with the unpruned B) and W are
+    contiguous m x n fp32 CUDA tensors on one device; W may be C_sparse or
+    C_dense itself."""
+    import torch
+    if C_dense.dim() != 2:
+        raise ValueError("C_dense must be 2-D")
+    m, n = C_dense.shape
+    _check_tensors(torch, W, [("C_sparse", C_sparse, torch.float32, m * n),
+                              ("C_dense", C_dense, torch.float32, m * n), ("W", W, torch.float32, m * n)])
+    if stream is None:
+        stream = torch.cuda.current_stream(W.device)
+    with torch.cuda.device(W.device):
+        st = lib().nmspmm_confusion(C_sparse.data_ptr(), C_dense.data_ptr(), W.data_ptr(), m, n,
+                                    stream.cuda_stream)
+    _check("nmspmm_confusion", st)
+    return W

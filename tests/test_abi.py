@@ -22,7 +22,7 @@ def declared_symbols():
 
 def test_library_exports_every_declared_symbol():
     names = declared_symbols()
-    assert len(names) == 16
+    assert len(names) == 17
     assert sorted(nm.EXPORTS) == names
     L = nm.lib()
     for name in names:
@@ -270,3 +270,18 @@ def test_gather_variant_list_matches_the_source():
     listed = listed[:listed.index("]\n")]
     tested = [tuple(int(x) for x in t) for t in re.findall(r"\((\d+), (\d+), (\d+), (\d+)\)", listed)]
     assert found and sorted(found) == sorted(tested)
+
+
+def test_confusion_argument_checks_without_a_launch():
+    """nmspmm_confusion (Eq. 2) refuses bad arguments before any HIP call, and
+    an empty matrix is a no-op."""
+    L = nm.lib()
+    p = 0x1000
+    assert L.nmspmm_confusion(p, p, p, -1, 4, None) == nm.NMSPMM_ERR_INVALID_ARG
+    assert L.nmspmm_confusion(p, p, p, 4, -1, None) == nm.NMSPMM_ERR_INVALID_ARG
+    assert L.nmspmm_confusion(None, None, None, 0, 5, None) == nm.NMSPMM_OK
+    assert L.nmspmm_confusion(p, p, p, 7, 0, None) == nm.NMSPMM_OK
+    assert L.nmspmm_confusion(None, p, p, 2, 2, None) == nm.NMSPMM_ERR_INVALID_ARG
+    assert L.nmspmm_confusion(p, p, None, 2, 2, None) == nm.NMSPMM_ERR_INVALID_ARG
+    assert L.nmspmm_confusion(p + 2, p, p, 2, 2, None) == nm.NMSPMM_ERR_UNSUPPORTED
+    assert L.nmspmm_confusion(p, p, p, 1 << 40, 1 << 40, None) == nm.NMSPMM_ERR_UNSUPPORTED

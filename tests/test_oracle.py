@@ -283,3 +283,72 @@ def test_epilogue_pins():
     assert abs(g[0, 3] - 0.8413447460685429) < 1e-15          # Phi(1)
     with pytest.raises(ValueError):
         oracle.epilogue(C, bias=np.zeros(3, np.float32))
+
+
+def test_eq2_hand_example():
+    """Eq. 2 on a hand-worked case: selection, Eq. 1 with its M/N factor,
+    the dense product and W, every value written out by hand."""
+    g = json.load(open(os.path.join(GOLDEN, "eq2_hand_example.json")))
+    N, M, V, m, k, n = g["N"], g["M"], g["V"], g["m"], g["k"], g["n"]
+    A = np.array(g["A"], np.float32)
+    B = np.array(g["B"], np.float32)
+    Bc, idx = oracle.compress(B, N, M, V)
+    assert np.array_equal(idx, np.array(g["idx"], np.uint8))
+    assert np.array_equal(Bc, np.array(g["Bc"], np.float32))
+    Cu = oracle.spmm(A, Bc, idx, m, n, k, N, M, V)
+    assert np.array_equal(Cu, np.array(g["C_sparse_unscaled"], np.float64))
+    Cs = oracle.epilogue(Cu, alpha=M / N)
+    assert np.array_equal(Cs, np.array(g["C_sparse"], np.float64))
+    C = oracle.dense(A, B)
+    assert np.array_equal(C, np.array(g["C_dense"], np.float64))
+    W = oracle.confusion(Cs, C)
+    assert np.array_equal(W, np.array(g["W_expected"], np.float64))
+
+
+@pytest.mark.parametrize("shape", TINY)
+def test_dense_matches_sequential_product_and_spmm_at_N_equals_M(shape):
+    """oracle_dense is the textbook product: bit for bit the sequential-k
+    fp64 sum, and bit for bit oracle_spmm on the N = M compression (every row
+    kept, the same order of additions)."""
+    m, k, n, _, M, V = shape
+    rng = np.random.default_rng(k * n + m)
+    A = rng.uniform(-1, 1, (m, k)).astype(np.float32)
+    B = rng.uniform(-1, 1, (k, n)).astype(np.float32)
+    C = oracle.dense(A, B)
+    assert np.array_equal(C, dense_sequential(A, B))
+    Bc, idx = oracle.compress(B, M, M, V)
+    assert np.array_equal(C, oracle.spmm(A, Bc, idx, m, n, k, M, M, V))
+    ref = A.astype(np.float64) @ B.astype(np.float64)   # library GEMM, its own order
+    assert np.allclose(C, ref, rtol=0, atol=1e-12 * np.abs(A).sum())
+
+
+@pytest.mark.parametrize("shape", TINY)
+def test_confusion_closed_form_on_pruned_B(shape):
+    """When B is already pruned, C = A*Bp and C' = (M/N)*A*Bp, so Eq. 2 has
+    the closed form W = (M/N - 1) * |A*Bp| / (m*n); at N = M it is zero."""
+    m, k, n, N, M, V = shape
+    A, Bp, _ = make_inputs(m, k, n, N, M, V, seed=41 + m + k)
+    Bc, idx = oracle.compress(Bp, N, M, V)
+    Cs = oracle.epilogue(oracle.spmm(A, Bc, idx, m, n, k, N, M, V), alpha=M / N)
+    W = oracle.confusion(Cs, oracle.dense(A, Bp))
+    AB = A.astype(np.float64) @ Bp.astype(np.float64)
+    ref = (M / N - 1.0) * np.abs(AB) / (m * n)
+    scale = (M / N + 1.0) * (np.abs(A).astype(np.float64) @ np.abs(Bp).astype(np.float64)) / (m * n)
+    assert np.all(np.abs(W - ref) <= 1e-12 * scale)
+    if N == M:
+        assert np.array_equal(W, np.zeros_like(W))
+
+
+def test_confusion_elementwise_properties():
+    """W is |difference| / (m*n): symmetric in its two arguments, zero on
+    equal inputs, and linear in a power-of-two scale (exact in binary)."""
+    rng = np.random.default_rng(3)
+    a = rng.standard_normal((5, 6))
+    b = rng.standard_normal((5, 6))
+    W = oracle.confusion(a, b)
+    assert np.array_equal(W, oracle.confusion(b, a))
+    assert np.array_equal(oracle.confusion(a, a), np.zeros_like(a))
+    assert np.array_equal(oracle.confusion(8 * a, 8 * b), 8 * W)
+    assert np.array_equal(oracle.confusion(np.array([[3.0]]), np.array([[-1.0]])), np.array([[4.0]]))
+    with pytest.raises(ValueError):
+        oracle.confusion(a, b[:, :5])

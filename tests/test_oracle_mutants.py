@@ -43,8 +43,17 @@ MUTANTS = {
     "alpha_dropped": ("double y = alpha * C[i * n + j];", "double y = C[i * n + j];"),
     "gelu_scale": ("erf(y / sqrt(2.0))", "erf(y / 2.0)"),
     "leaky_relu": ("y = y > 0.0 ? y : 0.0;", "y = y > 0.0 ? y : 0.01 * y;"),
+    # Eq. 2: the dense product drops its last k-row or reads B's rows reversed;
+    # W loses the absolute value or divides by m + n
+    "dense_dropped_term": ("for (int64_t kk = 0; kk < k; ++kk) {\n            const double av = (double)a[kk];",
+                           "for (int64_t kk = 0; kk + 1 < k; ++kk) {\n            const double av = (double)a[kk];"),
+    "dense_reversed_rows": ("const float *brow = B + kk * n;", "const float *brow = B + (k - 1 - kk) * n;"),
+    "confusion_signed": ("W[i * n + j] = fabs(Cs[i * n + j] - C[i * n + j]) / mn;",
+                         "W[i * n + j] = (Cs[i * n + j] - C[i * n + j]) / mn;"),
+    "confusion_norm": ("const double mn = (double)m * (double)n;", "const double mn = (double)m + (double)n;"),
 }
 EPILOGUE_MUTANTS = ("alpha_dropped", "gelu_scale", "leaky_relu")
+EQ2_MUTANTS = ("dense_dropped_term", "dense_reversed_rows", "confusion_signed", "confusion_norm")
 
 
 class _Lib:
@@ -57,7 +66,25 @@ class _Lib:
         L.oracle_spmm.argtypes = [F, F, U8, D, I64, I64, I64, I, I, I]
         L.oracle_compress.argtypes = [F, I64, I64, I, I, I, F, U8]
         L.oracle_epilogue.argtypes = [D, I64, I64, ctypes.c_double, F, I]
+        L.oracle_dense.argtypes = [F, F, D, I64, I64, I64]
+        L.oracle_confusion.argtypes = [D, D, D, I64, I64]
         self.L, self.F, self.D, self.U8 = L, F, D, U8
+
+    def dense(self, A, B):
+        A = np.ascontiguousarray(A, np.float32)
+        B = np.ascontiguousarray(B, np.float32)
+        C = np.zeros((A.shape[0], B.shape[1]), np.float64)
+        self.L.oracle_dense(A.ctypes.data_as(self.F), B.ctypes.data_as(self.F), C.ctypes.data_as(self.D),
+                            A.shape[0], B.shape[1], A.shape[1])
+        return C
+
+    def confusion(self, Cs, C):
+        Cs = np.ascontiguousarray(Cs, np.float64)
+        C = np.ascontiguousarray(C, np.float64)
+        W = np.zeros(C.shape, np.float64)
+        self.L.oracle_confusion(Cs.ctypes.data_as(self.D), C.ctypes.data_as(self.D), W.ctypes.data_as(self.D),
+                                C.shape[0], C.shape[1])
+        return W
 
     def epilogue(self, C, alpha, act):
         out = np.ascontiguousarray(C, np.float64).copy()
@@ -139,6 +166,20 @@ def failing_pins(lib):
         fails.append("epilogue_relu")
     if not np.allclose(lib.epilogue(C, 1.0, 2), C * norm.cdf(C), rtol=1e-13, atol=1e-15):
         fails.append("epilogue_gelu")
+    # Eq. 2: the dense product against the sequential product, and the
+    # hand-worked confusion matrix (golden)
+    rng = np.random.default_rng(12)
+    A = rng.uniform(-1, 1, (5, 12)).astype(np.float32)
+    B = rng.uniform(-1, 1, (12, 7)).astype(np.float32)
+    if not np.array_equal(lib.dense(A, B), _dense_sequential(A, B)):
+        fails.append("dense_brute_force")
+    g = json.load(open(os.path.join(GOLDEN, "eq2_hand_example.json")))
+    A, B = np.array(g["A"], np.float32), np.array(g["B"], np.float32)
+    N, M, V, m, k, n = g["N"], g["M"], g["V"], g["m"], g["k"], g["n"]
+    Bc, idx = lib.compress(B, N, M, V)
+    Cs = lib.epilogue(lib.spmm(A, Bc, idx, m, n, k, N, M, V), M / N, 0)
+    if not np.array_equal(lib.confusion(Cs, lib.dense(A, B)), np.array(g["W_expected"], np.float64)):
+        fails.append("eq2_hand_example")
     return fails
 
 
@@ -159,7 +200,7 @@ def test_every_planted_mistake_is_caught(tmp_path, source, name):
     # selection sites, in oracle_compress); only that one is changed
     at = source.find(old)
     assert at >= 0, f"mutation site for {name} not found"
-    if name not in ("keeps_smallest", "ties_to_larger") + EPILOGUE_MUTANTS:
+    if name not in ("keeps_smallest", "ties_to_larger") + EPILOGUE_MUTANTS + EQ2_MUTANTS:
         assert at < source.index("int oracle_bound(")
     src = tmp_path / f"mutant_{name}.c"
     src.write_text(source.replace(old, new, 1))
