@@ -23,6 +23,8 @@ int oracle_compress(const float *B, int64_t k, int64_t n, int N, int M, int V, f
 int oracle_decompress(const float *Bc, const uint8_t *idx, int64_t k, int64_t n, int N, int M, int V, float *B);
 int oracle_validate(const uint8_t *idx, int64_t k, int64_t n, int N, int M, int V);
 int oracle_epilogue(double *C, int64_t m, int64_t n, double alpha, const float *bias, int act);
+int oracle_dense(const float *A, const float *B, double *C, int64_t m, int64_t n, int64_t k);
+int oracle_confusion(const double *Cs, const double *C, double *W, int64_t m, int64_t n);
 }
 
 namespace {
@@ -114,6 +116,14 @@ void run_case(int64_t m, int64_t k, int64_t n, int N, int M, int V, bool dense_i
     expect(same, "product equals the dense brute force", k, n, N, M, V);
     std::vector<float> bias((size_t)n);
     for (auto &x : bias) x = uniform();
+    // Eq. 2: the dense product of the decompressed (pruned) B equals the
+    // sparse product, so W of the product against itself is zero
+    std::vector<double> Cd((size_t)(m * n)), W((size_t)(m * n));
+    expect(oracle_dense(A.data(), Bd.data(), Cd.data(), m, n, k) == 0, "oracle_dense", k, n, N, M, V);
+    expect(oracle_confusion(C.data(), Cd.data(), W.data(), m, n) == 0, "oracle_confusion", k, n, N, M, V);
+    bool zero = true;
+    for (size_t e = 0; e < W.size(); ++e) zero = zero && W[e] == 0.0;
+    expect(zero, "confusion of equal products is zero", k, n, N, M, V);
     for (int act = 0; act < 3; ++act)
         expect(oracle_epilogue(C.data(), m, n, 2.0, bias.data(), act) == 0, "oracle_epilogue", k, n, N, M, V);
 }
