@@ -344,6 +344,10 @@ bool parse_tuning(const char *spec, Tuning &t)
     return true;
 }
 
+// k short enough that the register-operand streaming kernel narrows its
+// column tiles to fill the grid (at most two A chunks of 16 rows).
+bool skinny_narrow_k(int64_t k) { return k <= 2 * skinny_chunk_cols(1); }
+
 // Streaming kernel for short products: every Bc value is loaded once per
 // 16 rows of C straight into MFMA operands and the A slice is staged in LDS;
 // k is split across workgroups until the grid has about one workgroup per CU.
@@ -369,6 +373,19 @@ bool plan_skinny(const float *A, const float *Bc, const float *C, int64_t m, int
     // else 128 (and split-k for the rest)
     const int64_t tiles_m = (m + skinny_rows(rt) - 1) / skinny_rows(rt);
     int cols = tiles_m * ((n + 255) / 256) >= 256 ? 256 : 128;
+    // A short k (each workgroup walks at most two A chunks): narrower
+    // columns instead, down to 32, while the grid stays within one workgroup
+    // per CU.  Each column tile re-reads the A slice from L2, which costs
+    // little at this k, and the fuller grid hides the load latency.  Measured
+    // on MI355X (graph replay): 256 x 256 x 256 at 16:32 8.4 -> 5.5 us (32
+    // columns), 512 x 512 x 512 at 16:32 10.3 -> 8.0 and at N = M 12.6 ->
+    // 10.2 (64), 256 x 512 x 1024 at 16:32 11.0 -> 8.6 (32), 128 x 2048 x 2048
+    // at 4:32 10.9 -> 8.7 (64), 16 x 8192 x 1024 at 4:32 8.1 -> 6.0 (32).
+    // Where k spans more chunks the split-k grid of 128 columns stays ahead
+    // (16 rows, k = n = 4096 at 4:32: 9.4 against 11.7 us; k = n = 8192:
+    // 14.3 against 19.0).
+    if (rt == 1 && skinny_narrow_k(k))
+        while (cols > 32 && tiles_m * ((n + cols / 2 - 1) / (cols / 2)) <= 256) cols /= 2;
     const int fc = t.skcols;
     if (fc == 32 || fc == 64 || fc == 128 || fc == 256) cols = fc;
     const int bv = std::min(bv_for(16, V), cols / 16);
@@ -494,9 +511,15 @@ Plan make_plan(const float *A, const float *Bc, const float *C, int64_t m, int64
         force_tile ? std::strcmp(force_tile, "skinny") == 0 : prefer_streaming(m, k, N, M);
     if (want_skinny) {
         // the PS override (tuning sweeps and tests): 0 never takes the
-        // pipelined streaming kernel, 1 takes it wherever it can run
+        // pipelined streaming kernel, 1 takes it wherever it can run.  By
+        // default it is not taken for up to 128 rows when k is short and
+        // 128-column tiles would not fill the chip: the register-operand
+        // kernel's narrowed tiles are faster there (128 x 2048 x 2048 at 4:32
+        // 12.3 -> 8.7 us, 64 x 2048 x 2048 10.8 -> 7.8).
         const int ps = t.ps;
-        if (ps != 0 && plan_stream(A, Bc, C, m, n, k, N, M, V, ps == 1, t, p)) return p;
+        const bool narrow_first = m <= 128 && skinny_narrow_k(k) && ((m + 15) / 16) * ((n + 127) / 128) < 256;
+        if ((ps == 1 || (ps < 0 && !narrow_first)) && plan_stream(A, Bc, C, m, n, k, N, M, V, ps == 1, t, p))
+            return p;
         if (plan_skinny(A, Bc, C, m, n, k, N, M, V, t, p)) return p;
     }
     p.kind = Kind::General;
@@ -614,6 +637,16 @@ bool plan_gather(const float *Bc, int64_t m, int64_t n, int64_t k, int N, int M,
     if (k * gather_rows(c.RT) * 4 >= (int64_t(1) << 31)) return false;
     if ((4 * nquads + 4 * 2 * 16 + 4) * n * 4 >= (int64_t(1) << 31)) return false;
     if ((n / V) * w >= (int64_t(1) << 29) || strips > (1 << 24)) return false;
+    // By default only where the strips alone fill the chip: its fixed costs
+    // (the transposition pass, two dependent loads before the first MFMA)
+    // pay off on long strips, and its split-k through partial strips loses
+    // to the streaming kernels.  Measured (graph replay, against the best
+    // streaming variant): 64 x 8192 x 8192 at 8:32 29.7 against 35.5 us,
+    // 128 x 8192 x 2048 at 4:32 15.7 against 18.9, 64 x 11008 x 4096 at 8:32
+    // 28.9 against 46.9; with split-k 128 x 4096 x 4096 at 4:32 20.8 against
+    // 17.1, 32 x 4096 x 4096 at 8:32 14.4 against 12.9, and on small products
+    // 128 x 512 x 512 at 16:32 14.1 against 6.5.
+    if (!force && strips < 256) return false;
     int64_t splits = 1;
     if (strips < 256)
         splits = std::max<int64_t>(1, std::min<int64_t>((256 + strips - 1) / strips, nquads / (8 * c.NW)));

@@ -158,9 +158,17 @@ def test_workspace_bytes():
     # the variants measured fastest on these shapes
     assert nm.nmspmm_kernel_name_ws(64, 8192, 8192, 4, 32, 64) == "nm_gather_kernel<r64,c32,w8,d4>+prep,split1"
     assert nm.nmspmm_kernel_name_ws(128, 8192, 8192, 4, 32, 64) == "nm_gather_kernel<r128,c32,w4,d4>+prep,split1"
-    # 32 strips of 32 columns, w = 2048: k split 8 ways (8 quads for each of 8 waves)
-    assert nm.nmspmm_workspace_bytes(20, 1024, 16384, 4, 32, 64) == 2 * MiB + 16 * 2048 * 4 + 32 * 8 * 32 * 32 * 4
-    assert nm.nmspmm_kernel_name_ws(20, 1024, 16384, 4, 32, 64) == "nm_gather_kernel<r32,c32,w8,d4>+prep,split8"
+    # forced onto 32 strips of 32 columns, w = 2048: k split 8 ways (8 quads
+    # for each of 8 waves)
+    gather = {"GATHER": 1}
+    assert nm.nmspmm_workspace_bytes(20, 1024, 16384, 4, 32, 64, tuning=gather) == \
+        2 * MiB + 16 * 2048 * 4 + 32 * 8 * 32 * 32 * 4
+    assert nm.nmspmm_kernel_name_ws(20, 1024, 16384, 4, 32, 64, tuning=gather) == \
+        "nm_gather_kernel<r32,c32,w8,d4>+prep,split8"
+    # by default strips that do not fill the chip keep the streaming kernels:
+    # 4 tiles of 32 x 256, k split 64 ways through the workspace
+    assert nm.nmspmm_kernel_name_ws(20, 1024, 16384, 4, 32, 64) == "nm_stream_kernel<r32,c256,bv2,rb16>+ws,split64"
+    assert nm.nmspmm_workspace_bytes(20, 1024, 16384, 4, 32, 64) == 4 * 64 * 32 * 256 * 4
     # 16 rows keep the register-operand streaming kernel (atomics, no workspace)
     assert nm.nmspmm_workspace_bytes(16, 8192, 8192, 4, 32, 64) == 0
     assert nm.nmspmm_workspace_bytes(16, 8192, 8192, 4, 32, 64, tuning={"GATHER": 1}) == MiB // 2 + MiB // 2
@@ -285,3 +293,31 @@ def test_confusion_argument_checks_without_a_launch():
     assert L.nmspmm_confusion(p, p, None, 2, 2, None) == nm.NMSPMM_ERR_INVALID_ARG
     assert L.nmspmm_confusion(p + 2, p, p, 2, 2, None) == nm.NMSPMM_ERR_UNSUPPORTED
     assert L.nmspmm_confusion(p, p, p, 1 << 40, 1 << 40, None) == nm.NMSPMM_ERR_UNSUPPORTED
+
+
+def test_dispatch_rules_for_short_products():
+    """The measured dispatch rules of the short products (host only).
+    - Register-operand streaming kernel, k of at most two A chunks: the
+      narrowest column tile (down to 32) whose grid stays within 256
+      workgroups; a longer k keeps 128 columns and splits k.
+    - Up to 128 rows with such a k and a grid that 128 columns would not fill:
+      that kernel rather than the pipelined one.
+    - The direct-gather kernel only where its strips alone fill the chip."""
+    name = nm.nmspmm_kernel_name
+    assert name(256, 256, 256, 16, 32, 32) == "nm_skinny_kernel<c32,bv2,qpw4>,split1"     # 128 workgroups
+    assert name(512, 512, 512, 16, 32, 32) == "nm_skinny_kernel<c64,bv2,qpw4>,split1"     # 256
+    assert name(512, 512, 512, 32, 32, 32) == "nm_skinny_kernel<c64,bv2,qpw4>,split1"
+    assert name(512, 1024, 1024, 16, 32, 32) == "nm_skinny_kernel<c128,bv2,qpw4>,split1"  # 256 at 128
+    assert name(256, 512, 1024, 16, 32, 32) == "nm_skinny_kernel<c32,bv2,qpw4>,split1"
+    assert name(16, 8192, 1024, 4, 32, 64) == "nm_skinny_kernel<c32,bv2,qpw4>,split1"
+    assert name(16, 8192, 8192, 4, 32, 64) == "nm_skinny_kernel<c128,bv4,qpw2>+zero,split4"  # long k
+    assert name(64, 2048, 2048, 4, 32, 64) == "nm_skinny_kernel<c32,bv2,qpw4>,split1"
+    assert name(128, 2048, 2048, 4, 32, 64) == "nm_skinny_kernel<c64,bv4,qpw4>,split1"
+    assert name(64, 2048, 4096, 4, 32, 64).startswith("nm_stream_kernel<")                 # k = 4096
+    assert name(512, 512, 512, 4, 32, 32).startswith("nm_stream_kernel<")                   # 512 rows
+    ws = nm.nmspmm_kernel_name_ws
+    assert ws(64, 8192, 8192, 4, 32, 64).startswith("nm_gather_kernel<")                    # 256 strips
+    assert ws(40, 8192, 1536, 4, 32, 64).startswith("nm_gather_kernel<r64,")
+    assert ws(128, 4096, 4096, 4, 32, 64).startswith("nm_stream_kernel<")                   # 128 strips
+    assert ws(128, 512, 512, 16, 32, 32).startswith("nm_skinny_kernel<c32,")
+    assert nm.nmspmm_workspace_bytes(128, 512, 512, 16, 32, 32) == 0

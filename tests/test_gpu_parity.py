@@ -591,7 +591,7 @@ def test_run_ws_graph_replay(gather):
     pass and the direct-gather kernel): every replay, with eager work between
     replays, gives the eager result bit for bit."""
     TUNE["GATHER"] = gather
-    m, k, n, N, M, V = 64, 2048, 2048, 4, 32, 64
+    m, k, n, N, M, V = 64, 4096, 2048, 4, 32, 64
     name = kname_ws(m, n, k, N, M, V)
     say(f"[graph] {name}")
     assert ("+ws,split" if gather == "0" else "nm_gather_kernel") in name

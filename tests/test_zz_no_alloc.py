@@ -26,8 +26,8 @@ import paper_2503_01253_amd as nm  # noqa: E402
 # streaming kernel, which takes no scratch at all.
 CASES = [
     (128, 8192, 8192, 4, 32, 64),
-    (64, 2048, 2048, 4, 32, 16),
-    (40, 1536, 512, 4, 32, 64),
+    (64, 4096, 2048, 4, 32, 16),
+    (40, 1536, 8192, 4, 32, 64),
     (16, 2048, 1024, 4, 32, 64),
 ]
 
