@@ -161,6 +161,11 @@ struct Plan {
     int CPW = 0, RB = 0, SW = 0;             // pipelined streaming kernel only
     int CT = 0, NW = 0, D = 0;               // direct-gather kernel only
     int64_t ws_bytes = 0;
+    // tiled kernel over two column regions (split-k off): columns [0,
+    // col_split) with `tile` as above, then [col_split, n) with tile2
+    const TileInfo *tile2 = nullptr;
+    int BV2 = 0, KA2 = 0, NQ2 = 0, stages2 = 0, tiles_n2 = 0;
+    int64_t col_split = 0;
 };
 
 bool aligned(const void *p, int bytes) { return (reinterpret_cast<uintptr_t>(p) % bytes) == 0; }
@@ -592,9 +597,72 @@ Plan make_plan(const float *A, const float *Bc, const float *C, int64_t m, int64
     // the thinnest products, where fewer, longer k slices stream better)
     const int64_t target = m <= 16 ? 128 : 256;
     int64_t splits = 1;
-    if (ntiles < target && stages > 1)
+    if (ntiles < target && stages > 1) {
         splits = std::min<int64_t>({(target + ntiles - 1) / ntiles, stages, 32});
+        // The 16-wave tiles run one workgroup per CU: a split that overflows
+        // one round leaves a partial second one, so they split only into
+        // whole rounds.  Measured on MI355X at 8:32, k = 4096 (graph replay):
+        // 1536 x 4096 on 192 tiles of 128 x 256 199.6 -> 165.0 us without
+        // the split, 2048 x 2816 on 176 tiles 196.5 -> 165.1.
+        if (tile->waves == 16) splits = std::max<int64_t>(1, std::min<int64_t>(splits, target / ntiles));
+    }
     if (t.splits >= 1) splits = std::min<int64_t>(t.splits, std::max<int64_t>(stages, 1));
+
+    // Two column regions where the sparse levels' wide 16-wave tile would
+    // need more than one round but the rest fits in one: whole 128 x 512
+    // column tiles for one round, then the remaining columns as one round of
+    // the 128 x 256 16-wave tile, a second launch, neither split.  Measured
+    // on MI355X (2048 x 11008 x 4096 at 8:32, per-launch events): the two
+    // regions alone take 284.9 us (2048 x 8192) and 165.1 us (2048 x 2816),
+    // against 474.8 us for the 128 x 256 8-wave tile over the whole grid
+    // (688 tiles, two per CU).
+    if (!force_tile && !ka_force && t.splits < 1 && 2 * N < M && V % 32 == 0 && m >= 1024 && n >= 1024) {
+        const TileInfo *big = tile_by_name("128x512m32w16"), *rest = tile_by_name("128x256m32w16");
+        const int64_t tm = (m + big->BM - 1) / big->BM;
+        const int64_t big_tiles = tm * ((n + big->BN - 1) / big->BN);
+        const int64_t cols1 = std::min<int64_t>(256 / tm, n / big->BN) * big->BN;
+        const int64_t tn2 = (n - cols1 + rest->BN - 1) / rest->BN;
+        auto fit = [&](const TileInfo *tl, int &bv_out, int &ka_out, int &nq_out) {
+            for (int bv = bv_for(tl->MI, V); bv >= 1; bv /= 2) {
+                if (!aligned(C, 4 * bv)) continue;
+                for (int i = 0; i < nka; ++i) {
+                    const int nq = stage_nq(ka_order[i], (ka_order[i] / M) * N);
+                    if (nq != 0 && tile_ok(*tl, bv, ka_order[i], nq, k, V)) {
+                        bv_out = bv;
+                        ka_out = ka_order[i];
+                        nq_out = nq;
+                        return true;
+                    }
+                }
+            }
+            return false;
+        };
+        int bv1 = 0, ka1 = 0, nq1 = 0, bv2 = 0, ka2 = 0, nq2 = 0;
+        // the second round must keep most of the chip busy (R4's keeps 176
+        // CUs): a nearly empty one costs a whole round's time
+        if (big_tiles > 256 && big_tiles <= 512 && cols1 > 0 && cols1 < n && cols1 % V == 0 && tm * tn2 <= 256 &&
+            tm * tn2 >= 160 &&
+            fit(big, bv1, ka1, nq1) && fit(rest, bv2, ka2, nq2)) {
+            p.kind = Kind::Tiled;
+            p.tile = big;
+            p.BV = bv1;
+            p.KA = ka1;
+            p.NQ = nq1;
+            p.RS = (ka1 / M) * N;
+            p.stages = (int)((groups + ka1 / M - 1) / (ka1 / M));
+            p.splits = 1;
+            p.tiles_m = (int)tm;
+            p.tiles_n = (int)(cols1 / big->BN);
+            p.tile2 = rest;
+            p.BV2 = bv2;
+            p.KA2 = ka2;
+            p.NQ2 = nq2;
+            p.stages2 = (int)((groups + ka2 / M - 1) / (ka2 / M));
+            p.tiles_n2 = (int)tn2;
+            p.col_split = cols1;
+            return p;
+        }
+    }
     p.kind = Kind::Tiled;
     p.tile = tile;
     p.BV = BV;
@@ -790,7 +858,14 @@ hipError_t launch_main(const Plan &p, const float *A, const float *Bc, const uin
     a.tiles_m = p.tiles_m;
     a.tiles_n = p.tiles_n;
     a.epi = epi;
-    return p.tile->launch(p.BV, p.KA, p.NQ, a, stream);
+    hipError_t e = p.tile->launch(p.BV, p.KA, p.NQ, a, stream);
+    if (e != hipSuccess || !p.tile2) return e;
+    // the second column region, with its own tile and stage depth
+    a.RS = (p.KA2 / M) * N;
+    a.stages = p.stages2;
+    a.tiles_n = p.tiles_n2;
+    a.col_begin = p.col_split;
+    return p.tile2->launch(p.BV2, p.KA2, p.NQ2, a, stream);
 }
 
 // The kernel(s) of a plan, then, when k was split across workgroups and the
@@ -835,7 +910,7 @@ const char *plan_name(const Plan &p, bool with_ws)
     case Kind::General: return "nm_general_kernel";
     case Kind::Tiled: case Kind::Skinny: case Kind::Stream: case Kind::Gather: break;
     }
-    thread_local char buf[96];
+    thread_local char buf[160];
     if (p.kind == Kind::Gather) {
         std::snprintf(buf, sizeof buf, "nm_gather_kernel<r%d,c%d,w%d,d%d>+prep,split%d", gather_rows(p.RT),
                       p.COLS, p.NW, p.D, p.splits);
@@ -858,6 +933,12 @@ const char *plan_name(const Plan &p, bool with_ws)
         else
             std::snprintf(buf, sizeof buf, "nm_skinny_kernel<c%d,bv%d,qpw%d,rows%d>%s%d", p.COLS, p.BV,
                           p.QPW, 16 * p.RT, p.splits > 1 ? "+zero,split" : ",split", p.splits);
+        return buf;
+    }
+    if (p.tile2) {
+        std::snprintf(buf, sizeof buf,
+                      "nm_tiled_kernel<%s,bv%d,ka%d,nq%d>,split1+cols%lld:nm_tiled_kernel<%s,bv%d,ka%d,nq%d>,split1",
+                      p.tile->name, p.BV, p.KA, p.NQ, (long long)p.col_split, p.tile2->name, p.BV2, p.KA2, p.NQ2);
         return buf;
     }
     std::snprintf(buf, sizeof buf, "nm_tiled_kernel<%s,bv%d,ka%d,nq%d>%s%d", p.tile->name, p.BV,

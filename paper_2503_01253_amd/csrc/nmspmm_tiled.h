@@ -158,6 +158,7 @@ struct TiledArgs {
     int splits;      // split-k factor (>1: atomic accumulation into a zeroed C)
     int tiles_m, tiles_n;
     Epilogue epi;    // applied by the stores when splits == 1
+    int64_t col_begin = 0;   // first column of the tile grid (a multiple of BN and of V)
 };
 
 // Workgroups are dispatched round-robin over the 8 XCDs.  Renumber them so
@@ -289,7 +290,7 @@ __global__ __launch_bounds__(T::NT) void nm_tiled_kernel(TiledArgs p)
     const int wave = T::MI == 32 ? __builtin_amdgcn_readfirstlane(tid >> 6) : tid >> 6;
     int tm, tn, split;
     map_tile(blockIdx.x, gridDim.x, p.tiles_m, p.tiles_n, tm, tn, split);
-    const int64_t row0 = (int64_t)tm * BM, col0 = (int64_t)tn * BN;
+    const int64_t row0 = (int64_t)tm * BM, col0 = p.col_begin + (int64_t)tn * BN;
     const int64_t m = p.m, n = p.n, k = p.k;
     const int N = p.N, M = p.M, V = p.V, RS = p.RS;
     const int64_t w = (k / M) * N, q = n / V;

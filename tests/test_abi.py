@@ -321,3 +321,23 @@ def test_dispatch_rules_for_short_products():
     assert ws(128, 4096, 4096, 4, 32, 64).startswith("nm_stream_kernel<")                   # 128 strips
     assert ws(128, 512, 512, 16, 32, 32).startswith("nm_skinny_kernel<c32,")
     assert nm.nmspmm_workspace_bytes(128, 512, 512, 16, 32, 32) == 0
+
+
+def test_dispatch_rules_for_tiled_grids():
+    """Host only.  The 16-wave tiles (one workgroup per CU) split k only into
+    whole rounds; the sparse levels' wide 16-wave tile takes two column
+    regions when it needs between one and two rounds and the rest of the
+    columns keep at least 160 CUs busy as one round of 128 x 256 tiles (R4)."""
+    name = nm.nmspmm_kernel_name
+    assert name(1536, 4096, 4096, 8, 32, 32) == "nm_tiled_kernel<128x256m32w16,bv1,ka64,nq4>,split1"   # 192 tiles
+    assert name(1536, 4096, 4096, 8, 32, 32, tuning={"TILE": "128x512m32w16"}).endswith("+zero,split2")  # 96
+    assert name(2048, 11008, 4096, 8, 32, 32) == (
+        "nm_tiled_kernel<128x512m32w16,bv1,ka64,nq4>,split1"
+        "+cols8192:nm_tiled_kernel<128x256m32w16,bv1,ka64,nq4>,split1")
+    assert "+cols8192:" in name(2048, 11008, 4096, 4, 32, 32)
+    assert "+cols" not in name(1536, 11008, 4096, 8, 32, 32)      # 12 tiles left for the second round
+    assert "+cols" not in name(2048, 11008, 4096, 16, 32, 32)     # 50 %: measured only below it
+    assert "+cols" not in name(4096, 4096, 4096, 8, 32, 32)       # one round
+    # a forced tile, stage depth or split keeps one region
+    assert "+cols" not in name(2048, 11008, 4096, 8, 32, 32, tuning={"SPLITS": 1})
+    assert nm.nmspmm_workspace_bytes(2048, 11008, 4096, 8, 32, 32) == 0

@@ -446,13 +446,30 @@ def test_dense_comparator_is_true_fp32():
 # streaming, streaming split-k, general kernel
 EPI_SHAPES = [
     (2048, 128, 8192, 8, 32, 32),
-    (64, 2048, 2048, 4, 32, 64),     # pipelined streaming kernel, split-k
+    (64, 4096, 2048, 4, 32, 64),     # pipelined streaming kernel, split-k
+    (8100, 160, 2784, 8, 32, 32),    # the tiled kernel over two column regions
     (512, 512, 512, 4, 32, 32),      # pipelined streaming kernel, fused epilogue
     (300, 256, 1088, 8, 32, 32),
     (16, 2048, 640, 4, 32, 128),
     (16, 512, 4096, 4, 32, 64),
     (17, 24, 10, 3, 8, 2),
 ]
+
+
+# The tiled kernel over two column regions (one round of whole 128 x 512
+# 16-wave tiles, then the rest as one round of 128 x 256 ones): rows past m,
+# a ragged last column tile, a partial last stage, V = 64.
+TWO_REGIONS = [(8100, 160, 2784, 8, 32, 32), (8192, 128, 2752, 4, 32, 64), (8192, 96, 2816, 8, 32, 32)]
+
+
+@pytest.mark.parametrize("shape", TWO_REGIONS, ids=lambda s: "x".join(map(str, s)))
+def test_two_column_regions_exact(shape):
+    m, k, n, N, M, V = shape
+    name = kname(m, n, k, N, M, V)
+    assert "+cols2048:nm_tiled_kernel<128x256m32w16," in name and name.startswith("nm_tiled_kernel<128x512m32w16,")
+    C, C_ref, _ = parity(m, k, n, N, M, V, "int", seed=7 + n)
+    assert bool(np.array_equal(C.astype(np.float64), C_ref)), \
+        f"{name}: {int(np.count_nonzero(C.astype(np.float64) != C_ref))} outputs differ"
 
 
 def run_ex(A, Bc, idx, m, n, k, N, M, V, alpha, bias, act):
