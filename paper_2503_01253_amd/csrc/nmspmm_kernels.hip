@@ -615,8 +615,10 @@ Plan make_plan(const float *A, const float *Bc, const float *C, int64_t m, int64
     // on MI355X (2048 x 11008 x 4096 at 8:32, per-launch events): the two
     // regions alone take 284.9 us (2048 x 8192) and 165.1 us (2048 x 2816),
     // against 474.8 us for the 128 x 256 8-wave tile over the whole grid
-    // (688 tiles, two per CU).
-    if (!force_tile && !ka_force && t.splits < 1 && 2 * N < M && V % 32 == 0 && m >= 1024 && n >= 1024) {
+    // (688 tiles, two per CU); at 4:32 260.3 against 362.8.  At 12:32 and
+    // 16:32 the 8-wave tile stays ahead (670 against 686 us, 832 against 858
+    // for the two regions timed alone).
+    if (!force_tile && !ka_force && t.splits < 1 && 4 * N <= M && V % 32 == 0 && m >= 1024 && n >= 1024) {
         const TileInfo *big = tile_by_name("128x512m32w16"), *rest = tile_by_name("128x256m32w16");
         const int64_t tm = (m + big->BM - 1) / big->BM;
         const int64_t big_tiles = tm * ((n + big->BN - 1) / big->BN);

@@ -325,7 +325,7 @@ def test_dispatch_rules_for_short_products():
 
 def test_dispatch_rules_for_tiled_grids():
     """Host only.  The 16-wave tiles (one workgroup per CU) split k only into
-    whole rounds; the sparse levels' wide 16-wave tile takes two column
+    whole rounds; at N/M <= 1/4 the wide 16-wave tile takes two column
     regions when it needs between one and two rounds and the rest of the
     columns keep at least 160 CUs busy as one round of 128 x 256 tiles (R4)."""
     name = nm.nmspmm_kernel_name
@@ -336,7 +336,8 @@ def test_dispatch_rules_for_tiled_grids():
         "+cols8192:nm_tiled_kernel<128x256m32w16,bv1,ka64,nq4>,split1")
     assert "+cols8192:" in name(2048, 11008, 4096, 4, 32, 32)
     assert "+cols" not in name(1536, 11008, 4096, 8, 32, 32)      # 12 tiles left for the second round
-    assert "+cols" not in name(2048, 11008, 4096, 16, 32, 32)     # 50 %: measured only below it
+    assert "+cols" not in name(2048, 11008, 4096, 16, 32, 32)     # measured slower at 50 %
+    assert "+cols" not in name(2048, 11008, 4096, 12, 32, 32)     # and at 62.5 %
     assert "+cols" not in name(4096, 4096, 4096, 8, 32, 32)       # one round
     # a forced tile, stage depth or split keeps one region
     assert "+cols" not in name(2048, 11008, 4096, 8, 32, 32, tuning={"SPLITS": 1})
