@@ -259,6 +259,9 @@ NMSPMM_API nmspmm_status_t nmspmm_run_noalloc(const float *A, const float *Bc, c
  *                              per wave and ring rows
  *   GATHER  0: never the direct-gather kernel, 1: wherever it runs
  *   GCT, GNW, GD               its column tiles, waves and ring depth
+ *   RG      0: never the row-gather kernel, 1: wherever it runs (up to 32
+ *           rows, V a multiple of 32)
+ *   RGCT, RGNW, RGD            its column tiles, waves and ring depth
  * A request the kernels cannot honour falls back to another kernel (a
  * forced tile that does not fit the shape: the general kernel).  An
  * unknown key or a malformed pair makes the call fail with

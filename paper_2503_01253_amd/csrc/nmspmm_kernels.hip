@@ -20,6 +20,7 @@
 #include "nmspmm.h"
 #include "nmspmm_gather.h"
 #include "nmspmm_internal.h"
+#include "nmspmm_rowgather.h"
 #include "nmspmm_skinny.h"
 #include "nmspmm_stream.h"
 #include "nmspmm_tiled.h"
@@ -151,7 +152,7 @@ const TileInfo *tile_by_name(const char *name)
     return nullptr;
 }
 
-enum class Kind { None, General, Tiled, Skinny, Stream, Gather };
+enum class Kind { None, General, Tiled, Skinny, Stream, Gather, RowGather };
 
 struct Plan {
     Kind kind = Kind::None;
@@ -307,6 +308,8 @@ struct Tuning {
     int psrt = 0, psbv = 0, pscpw = 0, psrb = 0;  // PSRT, PSBV, PSCPW, PSRB: its variant
     int gather = -1;             // GATHER: 0 never the direct-gather kernel, 1 wherever it runs
     int gct = 0, gnw = 0, gd = 0;  // GCT, GNW, GD: its variant
+    int rg = -1;                 // RG: 0 never the row-gather kernel, 1 wherever it runs
+    int rgct = 0, rgnw = 0, rgd = 0;  // RGCT, RGNW, RGD: its variant
     const char *tile_or_null() const { return tile[0] ? tile : nullptr; }
 };
 
@@ -338,7 +341,8 @@ bool parse_tuning(const char *spec, Tuning &t)
                 {"KA", &t.ka}, {"SPLITS", &t.splits}, {"QPW", &t.qpw}, {"SKCOLS", &t.skcols},
                 {"RT", &t.rt}, {"PS", &t.ps}, {"PSRT", &t.psrt}, {"PSBV", &t.psbv},
                 {"PSCPW", &t.pscpw}, {"PSRB", &t.psrb}, {"GATHER", &t.gather}, {"GCT", &t.gct},
-                {"GNW", &t.gnw}, {"GD", &t.gd}};
+                {"GNW", &t.gnw}, {"GD", &t.gd}, {"RG", &t.rg}, {"RGCT", &t.rgct}, {"RGNW", &t.rgnw},
+                {"RGD", &t.rgd}};
             bool found = false;
             for (const auto &f : fields)
                 if (std::strcmp(key, f.name) == 0) { *f.field = (int)v; found = true; }
@@ -506,6 +510,40 @@ bool plan_stream(const float *A, const float *Bc, const float *C, int64_t m, int
     return true;
 }
 
+// Row-gather kernel: up to 32 rows, one launch, every output written once.
+// By default for at most 4 rows where its 32-column strips alone fill the
+// chip: each quad then gathers at most 4 lines of A, and the single launch
+// beats the streaming kernel's zero fill and split-k atomics.  Measured on
+// MI355X (graph replay, against the register-operand streaming kernel with
+// split-k): k = n = 8192 at 4:32, V = 64: 1 row 13.0 -> 10.9 us, 2 rows 13.1
+// -> 11.3, 4 rows 13.2 -> 12.2; 4 x 11008 x 4096 at 8:32 27.4 -> 21.9.  From
+// 8 rows on the gathered lines cost more than the launch and atomics they
+// save (8 rows 13.4 against 13.9 us, 16 rows 14.2 against 18.0), and with
+// fewer strips the grid does not fill the chip (1 x 4096 x 4096 at 8:32,
+// V = 32: 9.9 against 10.2).  `force` (tuning sweeps and tests) takes it
+// wherever it can run.
+bool plan_rowgather(const float *A, const float *Bc, const float *C, int64_t m, int64_t n, int64_t k, int N,
+                    int M, int V, bool force, const Tuning &t, Plan &p)
+{
+    if (m > 32 || k == 0 || !aligned(A, 4) || !aligned(Bc, 16) || !aligned(C, 4)) return false;
+    if (!force && (m > 4 || n / 32 < 256)) return false;
+    RowGatherCfg c{m <= 16 ? 1 : 2, 2, 8, 4};
+    if (t.rgct) c.CT = t.rgct;
+    if (t.rgnw) c.NW = t.rgnw;
+    if (t.rgd) c.D = t.rgd;
+    if (!rowgather_fits(c, m, n, k, N, M, V)) return false;
+    p.kind = Kind::RowGather;
+    p.RT = c.RT;
+    p.CT = c.CT;
+    p.NW = c.NW;
+    p.D = c.D;
+    p.splits = 1;
+    p.tiles_m = 1;
+    p.COLS = 16 * c.CT;
+    p.tiles_n = (int)(n / p.COLS);
+    return true;
+}
+
 Plan make_plan(const float *A, const float *Bc, const float *C, int64_t m, int64_t n, int64_t k,
                int N, int M, int V, const Tuning &t)
 {
@@ -515,6 +553,7 @@ Plan make_plan(const float *A, const float *Bc, const float *C, int64_t m, int64
     const bool want_skinny =
         force_tile ? std::strcmp(force_tile, "skinny") == 0 : prefer_streaming(m, k, N, M);
     if (want_skinny) {
+        if (t.rg != 0 && plan_rowgather(A, Bc, C, m, n, k, N, M, V, t.rg == 1, t, p)) return p;
         // the PS override (tuning sweeps and tests): 0 never takes the
         // pipelined streaming kernel, 1 takes it wherever it can run.  By
         // default it is not taken for up to 128 rows when k is short and
@@ -823,6 +862,23 @@ hipError_t launch_main(const Plan &p, const float *A, const float *Bc, const uin
         g.ws = ws;
         return launch_gather(GatherCfg{p.RT, p.CT, p.NW, p.D}, g, stream);
     }
+    if (p.kind == Kind::RowGather) {
+        RowGatherArgs g;
+        g.A = A;
+        g.Bc = Bc;
+        g.idx = idx;
+        g.C = C;
+        g.m = m;
+        g.n = n;
+        g.k = k;
+        g.N = N;
+        g.M = M;
+        g.V = V;
+        g.epi = epi;
+        // Bc streamed past L2: at least 16 MB, four XCDs' worth
+        g.stream_b = (k / M) * N * n * 4 >= (int64_t(16) << 20) ? 1 : 0;
+        return launch_rowgather(RowGatherCfg{p.RT, p.CT, p.NW, p.D}, g, stream);
+    }
     if (p.kind == Kind::Stream) {
         StreamArgs s;
         s.A = A;
@@ -910,9 +966,13 @@ const char *plan_name(const Plan &p, bool with_ws)
     switch (p.kind) {
     case Kind::None: return "none";
     case Kind::General: return "nm_general_kernel";
-    case Kind::Tiled: case Kind::Skinny: case Kind::Stream: case Kind::Gather: break;
+    case Kind::Tiled: case Kind::Skinny: case Kind::Stream: case Kind::Gather: case Kind::RowGather: break;
     }
     thread_local char buf[160];
+    if (p.kind == Kind::RowGather) {
+        std::snprintf(buf, sizeof buf, "nm_rowgather_kernel<r%d,c%d,w%d,d%d>,split1", 16 * p.RT, p.COLS, p.NW, p.D);
+        return buf;
+    }
     if (p.kind == Kind::Gather) {
         std::snprintf(buf, sizeof buf, "nm_gather_kernel<r%d,c%d,w%d,d%d>+prep,split%d", gather_rows(p.RT),
                       p.COLS, p.NW, p.D, p.splits);

@@ -111,8 +111,19 @@ struct Shape {
     static constexpr int A_SLOTS = TWO_A ? 2 : 1;
     static constexpr int SLOT_BYTES = A_BYTES + BX_BYTES;
     static constexpr int LDS_BYTES = A_SLOTS * A_BYTES + NSLOT * BX_BYTES;
-    // A: 32 x 32 chunks, one per wave at a time, each thread a 4 x 4 block
-    static constexpr int A_CHUNKS = ((T::BM + 31) / 32) * (KA / 32);
+    // A: chunks of A_RP rows x 32 columns, one per wave at a time, each
+    // thread an (A_RP/8) x 4 block.  32-row chunks, or 16-row ones on the
+    // 16-wave tiles where 32-row chunks would leave three quarters of the
+    // waves without A work: the waves that load then load and store half as
+    // much, and they set the stage's pace.  Measured on MI355X (per-launch
+    // events): 2048 x 4096 x 4096 at 16:32 on 128 x 256 tiles (KA = 32)
+    // 317.4 -> 306.8 us; where 32-row chunks already kept half the waves busy
+    // (4096^3 at 16:32 and 8:32, 2048 x 4096 x 4096 at 8:32) it measured
+    // within -0.3 / +0.5 %.
+    static constexpr int A_CH32 = ((T::BM + 31) / 32) * (KA / 32);
+    static constexpr int A_RP = (T::NT >= 1024 && 4 * A_CH32 <= T::NW) ? 16 : 32;
+    static constexpr int A_RL = A_RP / 8;               // rows per thread
+    static constexpr int A_CHUNKS = ((T::BM + A_RP - 1) / A_RP) * (KA / 32);
     static constexpr int ACH = (A_CHUNKS + T::NW - 1) / T::NW;
     // B DMA: 16-byte pieces when the slab divides evenly, else dwords
     static constexpr int B_LANE = B_FLOATS * 4 / T::NT;
@@ -308,14 +319,16 @@ __global__ __launch_bounds__(T::NT) void nm_tiled_kernel(TiledArgs p)
 #pragma unroll
     for (int cg = 0; cg < NCG; ++cg) blk[cg] = (int)((col0 + wn * WN + cg * CG) / V - b_first);
 
-    // ---- A: global -> registers (4 x 4 blocks) -> LDS, k-major ----
-    // In a 32 x 32 chunk, lane l owns rows 4*(l%8)+t (t < 4) and columns
-    // 4*(l/8)..+3: each load instruction covers 8 rows x 128 bytes.
+    // ---- A: global -> registers (A_RL x 4 blocks) -> LDS, k-major ----
+    // In an A_RP x 32 chunk, lane l owns rows A_RL*(l%8)+t (t < A_RL) and
+    // columns 4*(l/8)..+3: each load instruction covers 8 rows x 128 bytes.
+    constexpr int A_RP = S::A_RP, A_RL = S::A_RL, A_PC = (BM + A_RP - 1) / A_RP;
+    typedef typename vec_of<A_RL>::type arvec;
     const int r8 = lane & 7, c8 = lane >> 3;
     const int rows_valid = (int)min64(BM, m - row0);
     const __amdgpu_buffer_rsrc_t a_rsrc =
         make_rsrc(p.A + row0 * k, (uint32_t)((int64_t)rows_valid * k * 4));
-    f32x4 ra[ACH][4];
+    f32x4 ra[ACH][A_RL];
     // `valid` false: the loads are still issued (so that every stage issues
     // the same memory instructions) but read zeros
     auto load_a = [&](int s, bool valid) {
@@ -323,11 +336,11 @@ __global__ __launch_bounds__(T::NT) void nm_tiled_kernel(TiledArgs p)
 #pragma unroll
         for (int ch = 0; ch < ACH; ++ch) {
             const int chunk = wave + ch * NW;
-            const int rbase = (chunk % ((BM + 31) / 32)) * 32, cbase = (chunk / ((BM + 31) / 32)) * 32;
+            const int rbase = (chunk % A_PC) * A_RP, cbase = (chunk / A_PC) * 32;
             const int64_t kcol = kc0 + cbase + 4 * c8;
 #pragma unroll
-            for (int t = 0; t < 4; ++t) {
-                const int r = rbase + 4 * r8 + t;
+            for (int t = 0; t < A_RL; ++t) {
+                const int r = rbase + A_RL * r8 + t;
                 const bool ok = valid && chunk < S::A_CHUNKS && r < BM && kcol < k;
                 const uint32_t off = ok ? (uint32_t)((r * k + kcol) * 4) : OOB;
                 // the buffer load returns raw dwords; reinterpret them as floats
@@ -340,12 +353,16 @@ __global__ __launch_bounds__(T::NT) void nm_tiled_kernel(TiledArgs p)
 #pragma unroll
         for (int ch = 0; ch < ACH; ++ch) {
             const int chunk = wave + ch * NW;
-            const int rbase = (chunk % ((BM + 31) / 32)) * 32, cbase = (chunk / ((BM + 31) / 32)) * 32;
-            if (chunk < S::A_CHUNKS && rbase + 4 * r8 < BM) {
+            const int rbase = (chunk % A_PC) * A_RP, cbase = (chunk / A_PC) * 32;
+            if (chunk < S::A_CHUNKS && rbase + A_RL * r8 < BM) {
 #pragma unroll
                 for (int c = 0; c < 4; ++c) {
-                    const f32x4 v = {ra[ch][0][c], ra[ch][1][c], ra[ch][2][c], ra[ch][3][c]};
-                    *reinterpret_cast<f32x4 *>(As + (cbase + 4 * c8 + c) * AST + rbase + 4 * r8) = v;
+                    arvec v;
+                    if constexpr (A_RL == 4)
+                        v = arvec{ra[ch][0][c], ra[ch][1][c], ra[ch][2][c], ra[ch][3][c]};
+                    else
+                        v = arvec{ra[ch][0][c], ra[ch][1][c]};
+                    *reinterpret_cast<arvec *>(As + (cbase + 4 * c8 + c) * AST + rbase + A_RL * r8) = v;
                 }
             }
         }
@@ -477,7 +494,7 @@ __global__ __launch_bounds__(T::NT) void nm_tiled_kernel(TiledArgs p)
 #pragma unroll
             for (int ch = 0; ch < ACH; ++ch)
 #pragma unroll
-                for (int t = 0; t < 4; ++t) ra[ch][t] = f32x4{nan, nan, nan, nan};
+                for (int t = 0; t < A_RL; ++t) ra[ch][t] = f32x4{nan, nan, nan, nan};
             store_a(cur ^ 1);
         }
         prep_offsets(cur);

@@ -274,7 +274,21 @@ def test_gather_variant_list_matches_the_source():
     block = block[:block.index("\n\n")]
     found = [tuple(int(x) for x in t) for t in re.findall(r"X\((\d+), (\d+), (\d+), (\d+)\)", block)]
     gpu = open(os.path.join(ROOT, "tests", "test_gpu_parity.py")).read()
-    listed = gpu[gpu.index("GATHER_VARIANTS = ["):]
+    listed = gpu[gpu.index("\nGATHER_VARIANTS = ["):]
+    listed = listed[:listed.index("]\n")]
+    tested = [tuple(int(x) for x in t) for t in re.findall(r"\((\d+), (\d+), (\d+), (\d+)\)", listed)]
+    assert found and sorted(found) == sorted(tested)
+
+
+def test_rowgather_variant_list_matches_the_source():
+    """The GPU tests force every row-gather instantiation; their list must be
+    the source's."""
+    src = open(os.path.join(ROOT, "paper_2503_01253_amd", "csrc", "nmspmm_rowgather.hip")).read()
+    block = src[src.index("#define NM_ROWGATHER_CONFIGS(X)"):]
+    block = block[:block.index("\n\n")]
+    found = [tuple(int(x) for x in t) for t in re.findall(r"X\((\d+), (\d+), (\d+), (\d+)\)", block)]
+    gpu = open(os.path.join(ROOT, "tests", "test_gpu_parity.py")).read()
+    listed = gpu[gpu.index("\nROWGATHER_VARIANTS = ["):]
     listed = listed[:listed.index("]\n")]
     tested = [tuple(int(x) for x in t) for t in re.findall(r"\((\d+), (\d+), (\d+), (\d+)\)", listed)]
     assert found and sorted(found) == sorted(tested)
@@ -302,7 +316,9 @@ def test_dispatch_rules_for_short_products():
       workgroups; a longer k keeps 128 columns and splits k.
     - Up to 128 rows with such a k and a grid that 128 columns would not fill:
       that kernel rather than the pipelined one.
-    - The direct-gather kernel only where its strips alone fill the chip."""
+    - The direct-gather kernel only where its strips alone fill the chip.
+    - The row-gather kernel for at most 4 rows where its 32-column strips
+      alone fill the chip."""
     name = nm.nmspmm_kernel_name
     assert name(256, 256, 256, 16, 32, 32) == "nm_skinny_kernel<c32,bv2,qpw4>,split1"     # 128 workgroups
     assert name(512, 512, 512, 16, 32, 32) == "nm_skinny_kernel<c64,bv2,qpw4>,split1"     # 256
@@ -321,6 +337,13 @@ def test_dispatch_rules_for_short_products():
     assert ws(128, 4096, 4096, 4, 32, 64).startswith("nm_stream_kernel<")                   # 128 strips
     assert ws(128, 512, 512, 16, 32, 32).startswith("nm_skinny_kernel<c32,")
     assert nm.nmspmm_workspace_bytes(128, 512, 512, 16, 32, 32) == 0
+    assert name(1, 8192, 8192, 4, 32, 64) == "nm_rowgather_kernel<r16,c32,w8,d4>,split1"   # 256 strips
+    assert name(4, 11008, 4096, 8, 32, 32) == "nm_rowgather_kernel<r16,c32,w8,d4>,split1"
+    assert ws(2, 8192, 8192, 4, 32, 64) == "nm_rowgather_kernel<r16,c32,w8,d4>,split1"
+    assert nm.nmspmm_workspace_bytes(2, 8192, 8192, 4, 32, 64) == 0
+    assert name(8, 8192, 8192, 4, 32, 64).startswith("nm_skinny_kernel<")                  # 8 rows
+    assert name(1, 4096, 4096, 8, 32, 32).startswith("nm_skinny_kernel<")                  # 128 strips
+    assert name(1, 8192, 8192, 4, 32, 16).startswith("nm_skinny_kernel<")                  # V = 16
 
 
 def test_dispatch_rules_for_tiled_grids():

@@ -745,6 +745,104 @@ def test_gather_kernel_chosen_by_rule():
     assert not kname_ws(4096, 4096, 4096, 16, 32, 32).startswith("nm_gather")
 
 
+# ---- row-gather kernel (one launch, at most 32 rows) ----
+ROWGATHER_SHAPES = [
+    (1, 512, 256, 4, 32, 32),        # one row
+    (5, 1024, 512, 2, 4, 32),        # M = 4: eight windows per A line
+    (16, 2048, 1024, 4, 32, 64),
+    (16, 776, 512, 3, 8, 32),        # w = 291: ragged last quad, quads span windows
+    (9, 1000, 512, 5, 8, 64),        # w = 625
+    (17, 4096, 2048, 1, 32, 64),     # N = 1 (no window division), 17 rows: two row tiles
+    (32, 2048, 1024, 16, 32, 32),    # 50 %, 32 rows
+    (20, 96, 128, 8, 32, 32),        # w = 24: six quads for eight waves
+    (12, 32, 256, 4, 32, 32),        # one window: one quad in all
+    (30, 256, 128, 32, 32, 32),      # N = M
+    (3, 2048, 256, 2, 32, 128),      # four strips per column block
+]
+
+
+def run_plain(A, Bc, idx, m, n, k, N, M, V, alpha=1.0, bias=None, act="none"):
+    dC = torch.full((m, n), float("nan"), dtype=torch.float32, device="cuda")
+    nm.nmspmm_run_ex(to_dev(A), to_dev(Bc), to_dev(idx), dC, m, n, k, N, M, V, alpha=alpha,
+                     bias=None if bias is None else to_dev(bias), act=act, tuning=TUNE)
+    torch.cuda.synchronize()
+    return dC.cpu().numpy()
+
+
+@pytest.mark.parametrize("shape", ROWGATHER_SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_rowgather_kernel_exact(shape):
+    """The row-gather kernel (forced): bit-exact on small integers, the
+    epilogue applied once and exactly, normal data within the bar and
+    bit-identical between runs."""
+    TUNE["RG"] = "1"
+    m, k, n, N, M, V = shape
+    name = kname(m, n, k, N, M, V)
+    say(f"[rowgather] {shape} {name}")
+    assert name.startswith("nm_rowgather_kernel<r%d," % (16 if m <= 16 else 32)), name
+    A, Bp, _ = make_inputs(m, k, n, N, M, V, 41 + m, "int")
+    Bc, idx = oracle.compress(Bp, N, M, V)
+    C_ref = oracle.spmm(A, Bc, idx, m, n, k, N, M, V)
+    C = run_plain(A, Bc, idx, m, n, k, N, M, V)
+    assert bool(np.array_equal(C.astype(np.float64), C_ref)), \
+        f"{int(np.count_nonzero(C.astype(np.float64) != C_ref))} outputs differ"
+    bias = np.random.default_rng(n).integers(-50, 50, n).astype(np.float32)
+    Y = run_plain(A, Bc, idx, m, n, k, N, M, V, alpha=4.0, bias=bias, act="relu")
+    assert bool(np.array_equal(Y.astype(np.float64), oracle.epilogue(C_ref, 4.0, bias, "relu")))
+    A, Bp, _ = make_inputs(m, k, n, N, M, V, 43 + m, "normal")
+    Bc, idx = oracle.compress(Bp, N, M, V)
+    C1 = run_plain(A, Bc, idx, m, n, k, N, M, V)
+    C2 = run_plain(A, Bc, idx, m, n, k, N, M, V)
+    assert bool(np.array_equal(C1.view(np.uint32), C2.view(np.uint32)))
+    r = oracle.check(C1, oracle.spmm(A, Bc, idx, m, n, k, N, M, V), oracle.bound(A, Bc, idx, m, n, k, N, M, V))
+    assert r, (name, r)
+
+
+@pytest.mark.parametrize("shape", [(1, 8192, 8192, 4, 32, 64), (3, 4096, 11008, 8, 32, 32),
+                                   (4, 2048, 8192, 16, 32, 32)], ids=lambda s: "x".join(map(str, s)))
+def test_rowgather_default_dispatch(shape):
+    """Decode batches of at most 4 rows take the row-gather kernel by default
+    (no workspace, no split): every output within the bar, and the same
+    result through the workspace entry point."""
+    m, k, n, N, M, V = shape
+    assert kname(m, n, k, N, M, V).startswith("nm_rowgather_kernel<r16,")
+    assert ws_bytes(m, n, k, N, M, V) == 0
+    C, C_ref, Bnd = parity(m, k, n, N, M, V, "normal", 61 + m)
+    r = oracle.check(C, C_ref, Bnd)
+    assert r, r
+
+
+# every instantiated variant {RT, CT, NW, D}; tests/test_abi.py checks this list against the source
+ROWGATHER_VARIANTS = [
+    (1, 2, 8, 4), (1, 2, 8, 8), (1, 2, 16, 4), (1, 2, 16, 8),
+    (1, 4, 8, 4), (1, 4, 8, 8), (1, 4, 16, 4), (1, 4, 16, 8),
+    (2, 2, 8, 4), (2, 2, 16, 4), (2, 4, 8, 4), (2, 4, 16, 4),
+]
+# per row-tile count: a ragged shape (w = 291, quads spanning windows) with V a multiple of 64
+ROWGATHER_VARIANT_SHAPES = {1: (13, 776, 512, 3, 8, 64), 2: (27, 776, 512, 3, 8, 64)}
+
+
+@pytest.mark.parametrize("variant", ROWGATHER_VARIANTS, ids=lambda v: "rt%d_ct%d_nw%d_d%d" % v)
+def test_rowgather_variants_exact(variant):
+    """Every row-gather instantiation, forced: bit-exact on small integers and
+    within the bar on normal data."""
+    rt, ct, nw, d = variant
+    for key, val in (("RG", 1), ("RGCT", ct), ("RGNW", nw), ("RGD", d)):
+        TUNE[key] = str(val)
+    m, k, n, N, M, V = ROWGATHER_VARIANT_SHAPES[rt]
+    name = kname(m, n, k, N, M, V)
+    say(f"[rowgather variant] {variant} {name}")
+    assert name == f"nm_rowgather_kernel<r{16 * rt},c{16 * ct},w{nw},d{d}>,split1"
+    A, Bp, _ = make_inputs(m, k, n, N, M, V, 47 + m, "int")
+    Bc, idx = oracle.compress(Bp, N, M, V)
+    C = run_plain(A, Bc, idx, m, n, k, N, M, V)
+    assert bool(np.array_equal(C.astype(np.float64), oracle.spmm(A, Bc, idx, m, n, k, N, M, V)))
+    A, Bp, _ = make_inputs(m, k, n, N, M, V, 53 + m, "normal")
+    Bc, idx = oracle.compress(Bp, N, M, V)
+    C = run_plain(A, Bc, idx, m, n, k, N, M, V)
+    r = oracle.check(C, oracle.spmm(A, Bc, idx, m, n, k, N, M, V), oracle.bound(A, Bc, idx, m, n, k, N, M, V))
+    assert r, (name, r)
+
+
 # ---- device packer (nmspmm_compress_device) ----
 PACK_SHAPES = [
     (64, 96, 4, 32, 32), (256, 256, 16, 32, 32), (128, 128, 8, 32, 64), (48, 30, 3, 8, 3),
