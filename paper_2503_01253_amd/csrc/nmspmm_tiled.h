@@ -378,7 +378,12 @@ __global__ __launch_bounds__(T::NT) void nm_tiled_kernel(TiledArgs p)
         b_ok[i] = col0 + col < n;
         b_off[i] = (uint32_t)(((int64_t)ul * n + col0 + col) * 4);
     }
-    const int x_ul = tid / QB, x_bl = tid % QB;
+    // X_s holds, per column block of the tile, the stage's offsets in the
+    // order a lane reads them: entry blk*RST + kq*NKS + ks is compressed row
+    // KG*ks + kq, so that one lane's NKS offsets are contiguous
+    constexpr int NKS_X = RST / (64 / T::MI);
+    const int x_bl = tid / RST, x_kq = (tid % RST) / NKS_X, x_ks = tid % NKS_X;
+    const int x_ul = (64 / T::MI) * x_ks + x_kq;
     const bool x_ok = tid < RST * QB && x_ul < RS && b_first + x_bl < q;
     const uint32_t x_off = (uint32_t)(x_ul * q + b_first + x_bl);
     auto dma_bx = [&](int s, int slot, bool valid) {
@@ -420,7 +425,7 @@ __global__ __launch_bounds__(T::NT) void nm_tiled_kernel(TiledArgs p)
 #pragma unroll
         for (int ks = 0; ks < NKS; ++ks)
 #pragma unroll
-            for (int cg = 0; cg < NCG; ++cg) aoff[ks][cg] = Xs[(KG * ks + kq) * QB + blk[cg]];
+            for (int cg = 0; cg < NCG; ++cg) aoff[ks][cg] = Xs[blk[cg] * RST + kq * NKS + ks];
 #pragma unroll
         for (int ks = 0; ks < NKS; ++ks) {
             // window of this compressed row inside the stage; padding rows
