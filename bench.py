@@ -44,8 +44,8 @@ CACHE_BYTES = 288 << 20      # 256 MB Infinity Cache + 8 x 4 MB L2
 # reads for a copy kernel of known size.  Keyed by workload, kernel variant
 # and the hash of that variant's device sources: null once any differs.
 TRAFFIC = {
-    ("R2", "nm_tiled_kernel<256x256m32w16,bv1,ka32,nq4>,split1", "b45432522e0bc5b4"): {
-        "fetch_kib": 132420.3, "fetch_factor": 1.99995,
+    ("R2", "nm_tiled_kernel<128x512m32w16,bv1,ka32,nq4>,split1", "2ce3526591e7b8bc"): {
+        "fetch_kib": 165186.8, "fetch_factor": 1.99995,
         "write_kib": 65536.0, "write_factor": 1.00000,
     },
 }
@@ -70,6 +70,8 @@ def kernel_source_sha(kernel_name):
         files.append("nmspmm_stream.hip")
     elif kernel_name.startswith("nm_gather_kernel<"):
         files.append("nmspmm_gather.hip")
+    elif kernel_name.startswith("nm_rowgather_kernel<"):
+        files.append("nmspmm_rowgather.hip")
     else:
         files.append("nmspmm_kernels.hip")
     h = hashlib.sha256()

@@ -239,11 +239,15 @@ double occupancy_of_grid(const TileInfo &t, int64_t m, int64_t n)
 //    128 x 128 tile (enough tiles to fill the chip, with split-k);
 //  * otherwise, at N/M <= 1/2 with V a multiple of 32, a 16-wave tile when
 //    its grid fills the chip in one round (at most 256 tiles, at least three
-//    quarters of the CUs busy): 256 x 256 at N/M = 1/2, 128 x 512 below,
+//    quarters of the CUs busy): 128 x 512, else (at N/M = 1/2) 256 x 256,
 //    else 128 x 256.  Four waves per SIMD hide the A loads of one wave behind
-//    the MFMAs of the others (R2 566 -> 543 us, R3c 184 -> 163 us); on grids
-//    of several rounds (2048 x 11008) and on split-k grids the 8-wave tiles
-//    measured faster;
+//    the MFMAs of the others (4096^3 at 16:32 566 -> 543 us, at 4:32 184 ->
+//    163 us); on grids of several rounds (2048 x 11008) and on split-k grids
+//    the 8-wave tiles measured faster.  At N/M = 1/2 the 128 x 512 tile,
+//    whose stage offsets come in 16-byte reads, measured ahead of 256 x 256
+//    (per-launch events, 4096^3 at 16:32 543.3 -> 530.8 us, 3072 x 4096 x
+//    4096 545 -> 531, 4096 x 2048 x 4096 281.7 -> 275.7, V = 64 547 -> 533);
+//    the 256 x 256 16-wave tile is still tried second;
 //  * else the 256 x 256 tile for dense-ish levels (N/M >= 1/2) and the
 //    128 x 512 tile with 32 x 32 MFMAs for the sparser ones, unless its grid
 //    would leave more than a quarter of the chip idle in the last wave, where
@@ -267,8 +271,8 @@ int preferences(int64_t m, int64_t n, int N, int M, int V, const TileInfo **out)
             const int64_t tiles = ((m + t.BM - 1) / t.BM) * ((n + t.BN - 1) / t.BN);
             return tiles <= 256 && occupancy_of_grid(t, m, n) >= 0.75;
         };
-        const char *wide = 2 * N == M ? "256x256m32w16" : "128x512m32w16";
-        if (one_round(wide)) add(wide);
+        if (one_round("128x512m32w16")) add("128x512m32w16");
+        else if (2 * N == M && one_round("256x256m32w16")) add("256x256m32w16");
         else if (one_round("128x256m32w16")) add("128x256m32w16");
     }
     const char *big = 2 * N >= M ? "256x256" : "128x512m32";
