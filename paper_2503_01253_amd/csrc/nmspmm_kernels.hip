@@ -190,10 +190,14 @@ int64_t plan_ws_bytes(const Plan &p)
 int stage_nq(int KA, int RS)
 {
     static const int shapes[][2] = {{32, 1}, {32, 2}, {32, 3}, {32, 4}, {32, 8},
-                                    {64, 2}, {64, 4}, {128, 1}, {128, 2}, {128, 4}};
+                                    {64, 2}, {64, 4}, {64, 8}, {128, 1}, {128, 2}, {128, 4}};
     int best = 0;
-    for (const auto &sh : shapes)
+    for (const auto &sh : shapes) {
+        // (64, 8) only for whole stages of 32 rows (the deep stages of the
+        // 16-wave tiles), never as padding
+        if (sh[0] == 64 && sh[1] == 8 && RS != 32) continue;
         if (sh[0] == KA && 4 * sh[1] >= RS && (best == 0 || sh[1] < best)) best = sh[1];
+    }
     return best;
 }
 
@@ -247,7 +251,11 @@ double occupancy_of_grid(const TileInfo &t, int64_t m, int64_t n)
 //    whose stage offsets come in 16-byte reads, measured ahead of 256 x 256
 //    (per-launch events, 4096^3 at 16:32 543.3 -> 530.8 us, 3072 x 4096 x
 //    4096 545 -> 531, 4096 x 2048 x 4096 281.7 -> 275.7, V = 64 547 -> 533);
-//    the 256 x 256 16-wave tile is still tried second;
+//    the 256 x 256 16-wave tile is still tried second.  At N = M (stages of
+//    32 compressed rows) the 16-wave tiles take the place of the 8-wave
+//    ones where they fill one round: 256 x 256 (4096^3 1029.7 -> 1025.5 us;
+//    128 x 512 measured 1038), else 128 x 256 (2048 x 4096 x 4096 564.2 ->
+//    554.7);
 //  * else the 256 x 256 tile for dense-ish levels (N/M >= 1/2) and the
 //    128 x 512 tile with 32 x 32 MFMAs for the sparser ones, unless its grid
 //    would leave more than a quarter of the chip idle in the last wave, where
@@ -265,14 +273,14 @@ int preferences(int64_t m, int64_t n, int N, int M, int V, const TileInfo **out)
         add("128x256m32"); add("128x128"); add("128x512"); add("256x256");
         return c;
     }
-    if (2 * N <= M && V % 32 == 0) {
+    if ((2 * N <= M || N == M) && V % 32 == 0) {
         auto one_round = [&](const char *name) {
             const TileInfo &t = *tile_by_name(name);
             const int64_t tiles = ((m + t.BM - 1) / t.BM) * ((n + t.BN - 1) / t.BN);
             return tiles <= 256 && occupancy_of_grid(t, m, n) >= 0.75;
         };
-        if (one_round("128x512m32w16")) add("128x512m32w16");
-        else if (2 * N == M && one_round("256x256m32w16")) add("256x256m32w16");
+        if (2 * N <= M && one_round("128x512m32w16")) add("128x512m32w16");
+        else if (2 * N >= M && one_round("256x256m32w16")) add("256x256m32w16");
         else if (one_round("128x256m32w16")) add("128x256m32w16");
     }
     const char *big = 2 * N >= M ? "256x256" : "128x512m32";
@@ -590,12 +598,19 @@ Plan make_plan(const float *A, const float *Bc, const float *C, int64_t m, int64
             if (KA % M == 0 && (KA / M) * N < min_rows) order[cnt++] = KA;
         return cnt;
     };
-    int ka_order[3], ka_small[3];
-    int nka = ka_list(16, ka_order), nks = ka_list(8, ka_small);
+    // The 16-wave tiles take stages of exactly 32 compressed rows where
+    // those fit (their 16-row A chunks leave the registers for them): half as
+    // many barriers per MFMA.  Measured (per-launch events): 2048 x 4096 x 4096 at
+    // 16:32 on 128 x 256 tiles 300.2 -> 292.0 us (KA = 64).
+    int ka_order[3], ka_small[3], ka_deep[4];
+    int nka = ka_list(16, ka_order), nks = ka_list(8, ka_small), nkd = 0;
+    for (int KA : {32, 64, 128})   // a whole stage of 32 rows, no padding, then the usual order
+        if (KA % M == 0 && (KA / M) * N == 32) ka_deep[nkd++] = KA;
+    for (int i = 0; i < nka; ++i) ka_deep[nkd++] = ka_order[i];
     const int ka_force = t.ka;
     if (ka_force == 32 || ka_force == 64 || ka_force == 128) {
-        ka_order[0] = ka_small[0] = ka_force;
-        nka = nks = 1;
+        ka_order[0] = ka_small[0] = ka_deep[0] = ka_force;
+        nka = nks = nkd = 1;
     }
 
     const TileInfo *cand[8];
@@ -617,8 +632,10 @@ Plan make_plan(const float *A, const float *Bc, const float *C, int64_t m, int64
         // CUs, so that a second workgroup per CU has work to bring
         const int64_t tiles_c = ((m + cand[j]->BM - 1) / cand[j]->BM) * ((n + cand[j]->BN - 1) / cand[j]->BN);
         const bool small = two_per_cu(*cand[j]) && tiles_c > 256;
-        const int *order = small ? ka_small : ka_order;
-        for (int i = 0; i < (small ? nks : nka) && !tile; ++i) {
+        const bool deep = cand[j]->waves == 16;
+        const int *order = small ? ka_small : deep ? ka_deep : ka_order;
+        const int norder = small ? nks : deep ? nkd : nka;
+        for (int i = 0; i < norder && !tile; ++i) {
             const int nq = stage_nq(order[i], (order[i] / M) * N);
             if (nq != 0 && tile_ok(*cand[j], bv, order[i], nq, k, V)) {
                 tile = cand[j];

@@ -121,7 +121,7 @@ struct Shape {
     // (4096^3 at 16:32 and 8:32, 2048 x 4096 x 4096 at 8:32) it measured
     // within -0.3 / +0.5 %.
     static constexpr int A_CH32 = ((T::BM + 31) / 32) * (KA / 32);
-    static constexpr int A_RP = (T::NT >= 1024 && 4 * A_CH32 <= T::NW) ? 16 : 32;
+    static constexpr int A_RP = (T::NT >= 1024 && (4 * A_CH32 <= T::NW || (NQ == 8 && A_CH32 <= T::NW))) ? 16 : 32;
     static constexpr int A_RL = A_RP / 8;               // rows per thread
     static constexpr int A_CHUNKS = ((T::BM + A_RP - 1) / A_RP) * (KA / 32);
     static constexpr int ACH = (A_CHUNKS + T::NW - 1) / T::NW;
@@ -131,7 +131,7 @@ struct Shape {
     static constexpr int B_CNT = B_LANE / B_W;
     // 16-wave tiles run four waves per SIMD, 128 VGPRs each: one A staging
     // chunk per wave and at most four quads per stage (more spill)
-    static constexpr bool REGS_OK = T::NT < 1024 || (NQ <= 4 && ACH == 1);
+    static constexpr bool REGS_OK = T::NT < 1024 || ((NQ <= 4 || (NQ == 8 && A_RP == 16)) && ACH == 1);
     static constexpr bool FITS = (TWO_A || ONE_A_OK) && REGS_OK && LDS_BYTES <= LDS_CAPACITY &&
                                  KA % 32 == 0 &&
                                  T::WN % CG == 0 && RST * QBMAX <= T::NT &&
@@ -575,7 +575,7 @@ hipError_t launch_tiled(const TiledArgs &a, hipStream_t stream)
 // The stage shapes instantiated: (KA, NQ), KA columns of A and 4*NQ padded
 // compressed rows per stage.
 #define NMSPMM_STAGE_SHAPES(X) \
-    X(32, 1) X(32, 2) X(32, 3) X(32, 4) X(32, 8) X(64, 2) X(64, 4) X(128, 1) X(128, 2) X(128, 4)
+    X(32, 1) X(32, 2) X(32, 3) X(32, 4) X(32, 8) X(64, 2) X(64, 4) X(64, 8) X(128, 1) X(128, 2) X(128, 4)
 
 template <class T, int BV>
 hipError_t launch_tiled_bv(int KA, int NQ, const TiledArgs &a, hipStream_t stream)
