@@ -20,6 +20,7 @@ from __future__ import annotations
 
 import argparse
 import ctypes
+import dataclasses
 import hashlib
 import json
 import os
@@ -44,8 +45,8 @@ CACHE_BYTES = 288 << 20      # 256 MB Infinity Cache + 8 x 4 MB L2
 # reads for a copy kernel of known size.  Keyed by workload, kernel variant
 # and the hash of that variant's device sources: null once any differs.
 TRAFFIC = {
-    ("R2", "nm_tiled_kernel<128x512m32w16,bv1,ka32,nq4>,split1", "2ce3526591e7b8bc"): {
-        "fetch_kib": 165186.8, "fetch_factor": 1.99995,
+    ("R2", "nm_tiled_kernel<128x512m32w16,bv1,ka32,nq4>,split1", "5fb63e6b0cb52a48"): {
+        "fetch_kib": 165176.3, "fetch_factor": 1.99995,
         "write_kib": 65536.0, "write_factor": 1.00000,
     },
 }
@@ -418,6 +419,17 @@ def measure_extras(torch, nm):
                             "frac_hbm_peak": moved / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS}
     del sets
     torch.cuda.empty_cache()
+    # decode batches of 1, 2 and 4 rows on the skinny shape (the row-gather
+    # kernel: one launch, A gathered from L2), graph replay; HBM-bound
+    dec = []
+    for mm in (1, 2, 4):
+        rr = dataclasses.replace(RUNS["R5a"], name=f"R5a@m={mm}", m=mm)
+        res, _ = measure(torch, nm, rr, 20, 3, False, graph=True)
+        gbs = rr.alg_bytes / (res["kernel_ms_median"] * 1e-3) / 1e9
+        dec.append({"m": mm, "kernel": res["kernel"], "us": round(res["kernel_ms_median"] * 1e3, 2),
+                    "alg_gb_s": round(gbs, 1), "frac_hbm_peak": round(gbs / PEAK_HBM_GBS, 3)})
+        torch.cuda.empty_cache()
+    out["decode_batches"] = {"workload": "m x 8192 x 8192 (m x n x k), 4:32, V=64, normal seed=1008", "runs": dec}
     return out
 
 

@@ -811,6 +811,34 @@ def test_rowgather_default_dispatch(shape):
     assert r, r
 
 
+def test_rowgather_graph_replay():
+    """The row-gather launch captured in a HIP graph (one kernel, nothing to
+    clear first): every replay, with eager work between replays, gives the
+    eager result bit for bit."""
+    m, k, n, N, M, V = 2, 4096, 8192, 4, 32, 64
+    name = kname(m, n, k, N, M, V)
+    say(f"[graph] {name}")
+    assert name.startswith("nm_rowgather_kernel<")
+    A, Bp, _ = make_inputs(m, k, n, N, M, V, 79, "normal")
+    Bc, idx = oracle.compress(Bp, N, M, V)
+    dA, dBc, didx = to_dev(A), to_dev(Bc), to_dev(idx)
+    dC = torch.empty((m, n), dtype=torch.float32, device="cuda")
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        nm.nmspmm_run(dA, dBc, didx, dC, m, n, k, N, M, V)
+    torch.cuda.synchronize()
+    eager = dC.cpu().numpy().copy()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        nm.nmspmm_run(dA, dBc, didx, dC, m, n, k, N, M, V)
+    for i in range(3):
+        dC.fill_(float("nan"))
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert bool(np.array_equal(dC.cpu().numpy().view(np.uint32), eager.view(np.uint32))), f"replay {i}"
+
+
 # every instantiated variant {RT, CT, NW, D}; tests/test_abi.py checks this list against the source
 ROWGATHER_VARIANTS = [
     (1, 2, 8, 4), (1, 2, 8, 8), (1, 2, 16, 4), (1, 2, 16, 8),
