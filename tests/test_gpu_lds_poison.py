@@ -67,6 +67,8 @@ TILES = ["256x256", "128x512", "128x128", "64x512", "16x512", "128x256", "256x12
 TILED_SHAPES = [
     (300, 256, 1088, 8, 32, 32),     # 8 windows, ragged m and n
     (130, 416, 1024, 4, 32, 64),     # 13 windows: a partial last stage at KA = 64 / 128
+    (300, 288, 1088, 16, 32, 32),    # 16:32: the 16-wave tiles' stages of 32 rows at KA = 64, a partial last one
+    (130, 192, 1024, 32, 32, 64),    # N = M: stages of 32 rows at KA = 32
 ]
 
 

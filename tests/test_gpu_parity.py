@@ -247,6 +247,8 @@ FORCED = [
     (130, 384, 1024, 4, 32, 64),
     (70, 128, 640, 16, 32, 128),
     (200, 96, 576, 12, 32, 64),
+    (130, 192, 1024, 32, 32, 64),    # N = M: the 16-wave tiles' stages of 32 rows
+    (300, 288, 1088, 16, 32, 32),    # 16:32 at KA = 64 on 128 x 256 (32-row stages), a partial last stage
 ]
 
 
