@@ -476,9 +476,11 @@ __global__ __launch_bounds__(T::NT) void nm_tiled_kernel(TiledArgs p)
 
     // ---- double-buffered stages, one barrier each ----
     // Stage i lives in LDS slot i % 2.  Its loads are issued while stage i-1
-    // is multiplied, after that stage's first MFMA K step: a wave whose
-    // memory instructions stall at issue then still has MFMAs in the pipe
-    // (issuing them before the first MFMA cost 5-12 % on MI355X).  Its A
+    // is multiplied, its A loads after that stage's first MFMA K step and its
+    // DMA after the second: a wave whose memory instructions stall at issue
+    // then still has MFMAs in the pipe (issuing them before the first MFMA
+    // cost 5-12 % on MI355X; splitting them over two K steps measured 4096^3
+    // at 16:32 530.7 -> 525.2 us, 2048 x 11008 x 4096 at 8:32 440.6 -> 434.1).  Its A
     // registers go to LDS at the end of stage i-1, and the barrier that
     // follows waits for them and for its DMA.  Every stage issues its loads
     // and its A store unconditionally (loads past the last stage read zeros),
@@ -512,10 +514,11 @@ __global__ __launch_bounds__(T::NT) void nm_tiled_kernel(TiledArgs p)
             __builtin_amdgcn_sched_barrier(0);
             mma(sl);
             __builtin_amdgcn_sched_barrier(0);
-            if (ks == 0) {
-                load_a(s_begin + it + 1, next);
-                dma_bx(s_begin + it + 1, cur ^ 1, next);
-            }
+            // the next stage's A loads after this stage's first K step, its
+            // DMA after the second: a wave's memory instructions then stall
+            // its issue for two shorter spells
+            if (ks == 0) load_a(s_begin + it + 1, next);
+            if (ks == (NKS > 1 ? 1 : 0)) dma_bx(s_begin + it + 1, cur ^ 1, next);
         }
         // one A_s slot: every wave must be done reading it
         if constexpr (!S::TWO_A) lds_sync();
