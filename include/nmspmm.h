@@ -18,9 +18,10 @@
  * factor).
  *
  * Every entry point is extern "C", returns a status code and never throws.
- * The library holds no global state (beyond the static scratch array of
- * nmspmm_run_noalloc and its per-device address) and is safe to call from
- * several host threads.
+ * The library's only global state is the static scratch array of
+ * nmspmm_run_noalloc (with its per-device address) and one memory pool per
+ * device for the workspaces of nmspmm_run and nmspmm_run_ex, created on
+ * first use; it is safe to call from several host threads.
  */
 #ifndef NMSPMM_H
 #define NMSPMM_H
@@ -89,14 +90,24 @@ NMSPMM_API nmspmm_status_t nmspmm_compress(const float *B_dense, int64_t k, int6
  *   idx: w x q uint8 row-major (read only)
  *   C  : m x n fp32 row-major, overwritten (must not alias the inputs)
  * Asynchronous on `stream` (NULL = the legacy default stream): the call
- * validates its arguments, enqueues the kernel(s) and returns; it allocates
- * nothing and does not synchronize.  Kernel faults surface at the caller's
- * next synchronization.  m == 0 or n == 0 returns NMSPMM_OK without a launch;
+ * validates its arguments, enqueues the kernel(s) and returns; it does not
+ * synchronize.  Kernel faults surface at the caller's next synchronization.
+ * Workspace: where nmspmm_run_ws would run the direct-gather kernel (the
+ * "+prep" names of nmspmm_kernel_name_ws), the call takes that kernel's
+ * workspace from a memory pool the library owns on the current device,
+ * allocated and released on `stream` around its kernels
+ * (hipMallocFromPoolAsync / hipFreeAsync; the pool keeps up to 256 MiB
+ * between calls), and the result is bit-identical to nmspmm_run_ws's.
+ * While `stream` is being captured into a graph, or when the pool cannot
+ * provide the memory, it runs the kernels that take none instead (named by
+ * nmspmm_kernel_name_tuned with with_workspace = 0), as it does for every
+ * other shape.  Callers that cannot allocate at all use nmspmm_run_noalloc.  m == 0 or n == 0 returns NMSPMM_OK without a launch;
  * k == 0 writes zeros to C.  Summation order: fp32 MFMA accumulation in an
  * order fixed by the kernel variant; when the variant splits k across
- * workgroups (the name from nmspmm_kernel_name ends in "+zero,splitS" with
- * S > 1) the partial tiles are added to C with fp32 atomics, so the last
- * bits of C may differ between runs.  idx contents are not validated on the device
+ * workgroups through atomics (the name from nmspmm_kernel_name ends in
+ * "+zero,splitS" with S > 1) the partial tiles are added to C with fp32
+ * atomics, so the last bits of C may differ between runs; through the
+ * workspace ("+ws,splitS") they are summed in a fixed order.  idx contents are not validated on the device
  * (use nmspmm_validate_idx on the host); an offset >= M is clamped to M-1
  * so that every access stays inside A, and the result is then unspecified.
  * Errors: NMSPMM_ERR_INVALID_ARG (bad shape, null pointer with non-empty
@@ -155,11 +166,13 @@ NMSPMM_API int64_t nmspmm_workspace_bytes(int64_t m, int64_t n, int64_t k, int N
  *              Either way: no zero fill of C, no atomics, and the result
  *              does not vary between runs.  Otherwise (NULL, smaller, or a
  *              shape whose kernel takes none) the call runs exactly as
- *              nmspmm_run_ex.
+ *              nmspmm_run_ex (which takes a pooled workspace where the
+ *              shape's kernel is the direct-gather kernel).
  * A workspace serves one call at a time: calls that overlap on one workspace
  * (on different streams) race.  Arguments, asynchrony and errors otherwise
  * as nmspmm_run_ex, plus NMSPMM_ERR_UNSUPPORTED for a workspace not aligned
- * to 256 bytes; the library allocates nothing. */
+ * to 256 bytes; with a large enough workspace the library allocates
+ * nothing. */
 NMSPMM_API nmspmm_status_t nmspmm_run_ws(const float *A, const float *Bc, const uint8_t *idx,
                               float *C, int64_t m, int64_t n, int64_t k, int N,
                               int M, int V, float alpha, const float *bias,
@@ -209,8 +222,10 @@ NMSPMM_API nmspmm_status_t nmspmm_validate_idx(const uint8_t *idx, int64_t k, in
 /* Static, never-null description of a status code. */
 NMSPMM_API const char *nmspmm_status_string(nmspmm_status_t s);
 
-/* Name of the kernel variant nmspmm_run would launch for this shape, assuming
- * buffers aligned as the allocator returns them: "none" when nothing is
+/* Name of the kernel variant nmspmm_run would launch for this shape outside
+ * graph capture (the direct-gather kernel with its pooled workspace where
+ * nmspmm_kernel_name_ws names it), assuming buffers aligned as the
+ * allocator returns them: "none" when nothing is
  * launched, "invalid" for a bad shape.  The string stays valid until the next
  * call from the same thread.  For benchmark and profile reports; it launches
  * nothing. */
@@ -267,15 +282,18 @@ NMSPMM_API nmspmm_status_t nmspmm_run_noalloc(const float *A, const float *Bc, c
  * unknown key or a malformed pair makes the call fail with
  * NMSPMM_ERR_INVALID_ARG ("invalid" / -1 for the two queries).  Arguments,
  * layout, asynchrony, workspace rules and errors otherwise as
- * nmspmm_run_ws. */
+ * nmspmm_run_ws, except that without a large enough workspace the call runs
+ * the kernels that take none (it takes no pooled workspace). */
 NMSPMM_API nmspmm_status_t nmspmm_run_tuned(const float *A, const float *Bc, const uint8_t *idx,
                                  float *C, int64_t m, int64_t n, int64_t k, int N,
                                  int M, int V, float alpha, const float *bias,
                                  nmspmm_act_t act, void *workspace, size_t workspace_bytes,
                                  const char *tuning, hipStream_t stream);
 
-/* nmspmm_kernel_name (with_workspace == 0) or nmspmm_kernel_name_ws
- * (otherwise) under the overrides of `tuning`. */
+/* Under the overrides of `tuning`: the kernels nmspmm_run_tuned launches
+ * without a workspace (with_workspace == 0; the tuned call takes no pooled
+ * workspace) or with one of nmspmm_workspace_bytes_tuned bytes (otherwise,
+ * as nmspmm_kernel_name_ws). */
 NMSPMM_API const char *nmspmm_kernel_name_tuned(int64_t m, int64_t n, int64_t k, int N, int M, int V,
                                      int with_workspace, const char *tuning);
 

@@ -309,6 +309,26 @@ def test_confusion_argument_checks_without_a_launch():
     assert L.nmspmm_confusion(p, p, p, 1 << 40, 1 << 40, None) == nm.NMSPMM_ERR_UNSUPPORTED
 
 
+def test_run_names_its_workspace_plan():
+    """nmspmm_kernel_name names what nmspmm_run launches outside graph
+    capture: the direct-gather kernel with a pooled workspace where
+    nmspmm_kernel_name_ws names it, the kernels that take no workspace
+    everywhere else (the tuned query without a workspace)."""
+    L = nm.lib()
+    for shape in [(64, 8192, 8192, 4, 32, 64), (128, 8192, 8192, 4, 32, 64), (40, 8192, 1536, 4, 32, 64)]:
+        assert nm.nmspmm_kernel_name(*shape) == nm.nmspmm_kernel_name_ws(*shape), shape
+        assert nm.nmspmm_kernel_name(*shape).startswith("nm_gather_kernel<"), shape
+    for shape in [(64, 2048, 4096, 4, 32, 16), (4096, 4096, 4096, 16, 32, 32), (16, 8192, 8192, 4, 32, 64),
+                  (1, 8192, 8192, 4, 32, 64)]:
+        assert nm.nmspmm_kernel_name(*shape) == L.nmspmm_kernel_name_tuned(*shape, 0, None).decode(), shape
+    assert L.nmspmm_kernel_name_tuned(64, 8192, 8192, 4, 32, 64, 0, None).decode() == \
+        "nm_stream_kernel<r32,c256,bv2,rb16>+zero,split4"
+    # m = 64, n = 2048, k = 4096, V = 16: the pipelined streaming kernel splits
+    # k; with a workspace through it, nmspmm_run through atomics
+    assert nm.nmspmm_kernel_name_ws(64, 2048, 4096, 4, 32, 16) == "nm_stream_kernel<r32,c128,bv1,rb16>+ws,split8"
+    assert nm.nmspmm_kernel_name(64, 2048, 4096, 4, 32, 16) == "nm_stream_kernel<r32,c128,bv1,rb16>+zero,split8"
+
+
 def test_dispatch_rules_for_short_products():
     """The measured dispatch rules of the short products (host only).
     - Register-operand streaming kernel, k of at most two A chunks: the

@@ -418,9 +418,12 @@ def test_stream_kernel_chosen_by_rule():
     """The dispatcher takes the pipelined kernel for the sparse levels (ring of
     16 or 32 rows) above 16 rows: 32-row tiles with split-k for short
     products, the largest tile that fills the chip for taller ones; and keeps
-    the register-operand kernel for 16-row decode shapes and denser levels."""
+    the register-operand kernel for 16-row decode shapes and denser levels
+    (R5b's shape, whose default with a workspace is the direct-gather kernel:
+    the kernels that take none)."""
     TUNE.pop("PS", None)
-    assert kname(64, 8192, 8192, 4, 32, 64) == "nm_stream_kernel<r32,c256,bv2,rb16>+zero,split4"
+    assert nm.lib().nmspmm_kernel_name_tuned(64, 8192, 8192, 4, 32, 64, 0, None).decode() == \
+        "nm_stream_kernel<r32,c256,bv2,rb16>+zero,split4"
     assert kname(1024, 2048, 2048, 4, 32, 32) == "nm_stream_kernel<r32,c256,bv2,rb16>,split1"
     assert kname(512, 2048, 2048, 8, 32, 32) == "nm_stream_kernel<r16,c256,bv2,rb32>,split1"
     assert kname(512, 512, 512, 4, 32, 32) == "nm_stream_kernel<r16,c128,bv1,rb16>,split1"
@@ -633,6 +636,107 @@ def test_run_ws_graph_replay(gather):
         g.replay()
         torch.cuda.synchronize()
         assert bool(np.array_equal(dC.cpu().numpy().view(np.uint32), eager.view(np.uint32))), f"replay {i}"
+
+
+# ---- pooled workspaces of nmspmm_run / nmspmm_run_ex ----
+POOLED_SHAPES = [
+    (64, 8192, 8192, 4, 32, 64),    # R5b
+    (128, 2048, 8192, 4, 32, 64),   # 128 rows
+    (40, 1536, 8192, 4, 32, 64),    # 40 rows in the 64-row variant
+]
+
+
+@pytest.mark.parametrize("shape", POOLED_SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_run_takes_pooled_workspace(shape):
+    """Outside graph capture nmspmm_run and nmspmm_run_ex take the direct-
+    gather kernel with a workspace from the library's pool where
+    nmspmm_run_ws would run it: the name is that of nmspmm_kernel_name_ws, and
+    the output is bit-identical to nmspmm_run_ws's (with and without the
+    epilogue), twice in a row, and within the bar."""
+    m, k, n, N, M, V = shape
+    name = nm.nmspmm_kernel_name(m, n, k, N, M, V)
+    say(f"[pooled] {shape} {name}")
+    assert name == nm.nmspmm_kernel_name_ws(m, n, k, N, M, V)
+    assert name.startswith("nm_gather_kernel<")
+    A, Bp, _ = make_inputs(m, k, n, N, M, V, 51 + m, "normal")
+    Bc, idx = oracle.compress(Bp, N, M, V)
+    dA, dBc, didx = to_dev(A), to_dev(Bc), to_dev(idx)
+    ws = new_workspace(m, n, k, N, M, V)
+    bias = torch.randn(n, device="cuda")
+    for kw in ({}, {"alpha": M / N, "bias": bias, "act": "gelu"}):
+        ref = torch.full((m, n), float("nan"), device="cuda")
+        nm.nmspmm_run_ws(dA, dBc, didx, ref, m, n, k, N, M, V, ws, **kw)
+        for _ in range(2):
+            out = torch.full((m, n), float("nan"), device="cuda")
+            if kw:
+                nm.nmspmm_run_ex(dA, dBc, didx, out, m, n, k, N, M, V, **kw)
+            else:
+                nm.nmspmm_run(dA, dBc, didx, out, m, n, k, N, M, V)
+            torch.cuda.synchronize()
+            assert torch.equal(out.view(torch.int32), ref.view(torch.int32))
+    out = torch.full((m, n), float("nan"), device="cuda")
+    nm.nmspmm_run(dA, dBc, didx, out, m, n, k, N, M, V)
+    torch.cuda.synchronize()
+    r = oracle.check(out.cpu().numpy(), oracle.spmm(A, Bc, idx, m, n, k, N, M, V),
+                     oracle.bound(A, Bc, idx, m, n, k, N, M, V))
+    assert r, (name, r)
+
+
+def test_run_under_capture_takes_no_workspace():
+    """Captured into a HIP graph, nmspmm_run allocates nothing: it records the
+    kernels that take no workspace (split-k with a fill kernel and atomics),
+    and every replay, with eager work between replays, meets the bar."""
+    m, k, n, N, M, V = 64, 4096, 8192, 4, 32, 64
+    no_ws = nm.lib().nmspmm_kernel_name_tuned(m, n, k, N, M, V, 0, None).decode()
+    say(f"[capture] {nm.nmspmm_kernel_name(m, n, k, N, M, V)} / under capture {no_ws}")
+    assert "+prep" not in no_ws and "+ws" not in no_ws
+    A, Bp, _ = make_inputs(m, k, n, N, M, V, 61, "normal")
+    Bc, idx = oracle.compress(Bp, N, M, V)
+    dA, dBc, didx = to_dev(A), to_dev(Bc), to_dev(idx)
+    C_ref = oracle.spmm(A, Bc, idx, m, n, k, N, M, V)
+    Bnd = oracle.bound(A, Bc, idx, m, n, k, N, M, V)
+    dC = torch.empty((m, n), dtype=torch.float32, device="cuda")
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        nm.nmspmm_run(dA, dBc, didx, dC, m, n, k, N, M, V)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        nm.nmspmm_run(dA, dBc, didx, dC, m, n, k, N, M, V)
+    for i in range(3):
+        dC.fill_(float("nan"))
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert oracle.check(dC.cpu().numpy(), C_ref, Bnd), f"replay {i}"
+        eager = torch.full((m, n), float("nan"), device="cuda")
+        nm.nmspmm_run(dA, dBc, didx, eager, m, n, k, N, M, V)
+        torch.cuda.synchronize()
+        assert oracle.check(eager.cpu().numpy(), C_ref, Bnd)
+
+
+def test_run_pooled_workspaces_on_two_streams():
+    """Calls on two streams at once each take their own pooled workspace: both
+    outputs bit-identical to nmspmm_run_ws's."""
+    m, k, n, N, M, V = 64, 8192, 8192, 4, 32, 64
+    A, Bp, _ = make_inputs(m, k, n, N, M, V, 71, "normal")
+    Bc, idx = oracle.compress(Bp, N, M, V)
+    dA, dBc, didx = to_dev(A), to_dev(Bc), to_dev(idx)
+    A2 = torch.randn((m, k), device="cuda")
+    ref = [torch.empty((m, n), device="cuda") for _ in range(2)]
+    ws = new_workspace(m, n, k, N, M, V)
+    for a, r in zip((dA, A2), ref):
+        nm.nmspmm_run_ws(a, dBc, didx, r, m, n, k, N, M, V, ws)
+    torch.cuda.synchronize()
+    outs = [torch.full((m, n), float("nan"), device="cuda") for _ in range(2)]
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    for _ in range(3):
+        for a, o, st in zip((dA, A2), outs, streams):
+            with torch.cuda.stream(st):
+                nm.nmspmm_run(a, dBc, didx, o, m, n, k, N, M, V, stream=st)
+        torch.cuda.synchronize()
+        for o, r in zip(outs, ref):
+            assert torch.equal(o.view(torch.int32), r.view(torch.int32))
 
 
 # ---- direct-gather kernel (nmspmm_run_ws on short products) ----
