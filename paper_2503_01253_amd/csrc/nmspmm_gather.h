@@ -19,6 +19,7 @@ struct GatherArgs {
     int64_t m, n, k;
     int N, M, V;
     int splits;      // workgroups per column strip along the compressed rows
+    int halves;      // row halves (1 or 2, splits == 1 only): each a workgroup of 16*RT rows
     Epilogue epi;    // applied by the stores when splits == 1
     void *ws;        // workspace of gather_layout(...).total bytes, 256-byte aligned
 };
@@ -28,6 +29,7 @@ struct GatherArgs {
 // per wave.
 struct GatherCfg {
     int RT, CT, NW, D;
+    int H = 1;       // row halves of 16*RT rows each (splits == 1 only)
 };
 
 int gather_rows(int RT);  // 16 * RT

@@ -24,6 +24,7 @@
 // fixed order.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cstdint>
 
 #include "nmspmm_gather.h"
@@ -52,6 +53,13 @@ __global__ __launch_bounds__(256) void nm_gather_prep_kernel(const float *__rest
 {
     __shared__ float t[ROWS * (TK + 1)];
     __shared__ int32_t o[64 * (OU + 1)];
+    // row half blockIdx.y (its own At of ROWS-float rows; the offset blocks
+    // run once, in half 0)
+    const int h = (int)blockIdx.y;
+    if (h > 0 && (int)blockIdx.x >= tblocks) return;
+    A += (int64_t)h * ROWS * k;
+    At += (int64_t)h * k * ROWS;
+    m = max(0, min(ROWS, m - h * ROWS));
     if (VEC && (int)blockIdx.x < tblocks) {
         // ROWS x TK/4 pieces of 4 columns in, TK x ROWS/4 pieces of 4 rows out
         constexpr int PIECES = ROWS * TK / 4, PER = (PIECES + 255) / 256;
@@ -215,7 +223,7 @@ template <int RT, int CT, int NW, int D>
 __global__ __launch_bounds__(NW * 64) void nm_gather_kernel(
     const float *__restrict__ At, const int32_t *__restrict__ off, const float *__restrict__ Bc,
     float *__restrict__ C, float *__restrict__ part, int m, int64_t n, int k, int w, int V, int strips,
-    int splits, Epilogue epi)
+    int splits, int halves, Epilogue epi)
 {
     using S = GShape<RT, CT, NW>;
     constexpr int ROWS = S::ROWS, COLS = S::COLS, RST = S::RST;
@@ -229,7 +237,13 @@ __global__ __launch_bounds__(NW * 64) void nm_gather_kernel(
     const int nwg = gridDim.x, pid = blockIdx.x;
     const int xcd = pid % 8, local = pid / 8, full = nwg / 8, rem = nwg % 8;
     const int logical = xcd < rem ? xcd * (full + 1) + local : rem * (full + 1) + (xcd - rem) * full + local;
-    const int split = logical / strips, strip = logical - split * strips;
+    // the row halves of one strip are consecutive (one XCD: they share its
+    // Bc lines in L2); each has its own At of ROWS-float rows
+    const int h = logical % halves, rest = logical / halves;
+    const int split = rest / strips, strip = rest - split * strips;
+    At += (int64_t)h * k * ROWS;
+    C += (int64_t)h * ROWS * n;
+    m = max(0, min(ROWS, m - h * ROWS));
     const int64_t j0 = (int64_t)strip * COLS;
     const int b = (int)(j0 / V);
     const int nquads = (w + 3) / 4;
@@ -330,7 +344,8 @@ template <int RT, int CT, int NW, int D>
 hipError_t launch_cfg(const GatherArgs &a, hipStream_t stream)
 {
     constexpr int ROWS = 16 * RT, COLS = 16 * CT;
-    const GatherCfg cfg{RT, CT, NW, D};
+    GatherCfg cfg{RT, CT, NW, D};
+    cfg.H = a.halves;
     const int w = (int)(a.k / a.M * a.N), q = (int)(a.n / a.V), strips = (int)(a.n / COLS);
     const GatherLayout L = gather_layout(cfg, a.n, a.k, a.N, a.M, a.V, a.splits);
     char *base = static_cast<char *>(a.ws);
@@ -338,18 +353,19 @@ hipError_t launch_cfg(const GatherArgs &a, hipStream_t stream)
     int32_t *off = reinterpret_cast<int32_t *>(base + L.off);
     float *part = a.splits > 1 ? reinterpret_cast<float *>(base + L.part) : nullptr;
     const int tblocks = (int)((a.k + TK - 1) / TK), ublocks = (w + OU - 1) / OU, bblocks = (q + 63) / 64;
+    const int H = a.splits == 1 ? max(1, a.halves) : 1;
     if (a.k % 4 == 0 && reinterpret_cast<uintptr_t>(a.A) % 16 == 0)
-        hipLaunchKernelGGL((nm_gather_prep_kernel<ROWS, true>), dim3((unsigned)(tblocks + ublocks * bblocks)),
+        hipLaunchKernelGGL((nm_gather_prep_kernel<ROWS, true>), dim3((unsigned)(tblocks + ublocks * bblocks), H),
                            dim3(256), 0, stream, a.A, a.idx, At, off, (int)a.m, (int)a.k, w, q, a.N, a.M, tblocks,
                            ublocks);
     else
-        hipLaunchKernelGGL((nm_gather_prep_kernel<ROWS, false>), dim3((unsigned)(tblocks + ublocks * bblocks)),
+        hipLaunchKernelGGL((nm_gather_prep_kernel<ROWS, false>), dim3((unsigned)(tblocks + ublocks * bblocks), H),
                            dim3(256), 0, stream, a.A, a.idx, At, off, (int)a.m, (int)a.k, w, q, a.N, a.M, tblocks,
                            ublocks);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((nm_gather_kernel<RT, CT, NW, D>), dim3((unsigned)(strips * a.splits)), dim3(NW * 64), 0,
-                       stream, At, off, a.Bc, a.C, part, (int)a.m, a.n, (int)a.k, w, a.V, strips, a.splits,
+    hipLaunchKernelGGL((nm_gather_kernel<RT, CT, NW, D>), dim3((unsigned)(strips * a.splits * H)), dim3(NW * 64),
+                       0, stream, At, off, a.Bc, a.C, part, (int)a.m, a.n, (int)a.k, w, a.V, strips, a.splits, H,
                        a.epi);
     return hipGetLastError();
 }
@@ -376,11 +392,12 @@ bool gather_has(const GatherCfg &c)
 
 GatherLayout gather_layout(const GatherCfg &c, int64_t n, int64_t k, int N, int M, int V, int splits)
 {
+    const int64_t halves = splits == 1 ? std::max(1, c.H) : 1;
     auto up = [](int64_t x) { return (x + 255) / 256 * 256; };
     const int64_t w = k / M * N, q = n / V, strips = n / (16 * c.CT);
     GatherLayout L;
     L.at = 0;
-    L.off = up(k * 16 * c.RT * 4);
+    L.off = up(halves * k * 16 * c.RT * 4);
     L.part = L.off + up(q * w * 4);
     L.total = L.part + (splits > 1 ? up(strips * splits * 16 * c.RT * 16 * c.CT * 4) : 0);
     return L;

@@ -161,6 +161,7 @@ struct Plan {
     int QPW = 0, COLS = 0, CW = 0, RT = 1;   // streaming kernels only
     int CPW = 0, RB = 0, SW = 0;             // pipelined streaming kernel only
     int CT = 0, NW = 0, D = 0;               // direct-gather kernel only
+    int H = 1;                               // its row halves
     int64_t ws_bytes = 0;
     // tiled kernel over two column regions (split-k off): columns [0,
     // col_split) with `tile` as above, then [col_split, n) with tile2
@@ -320,6 +321,7 @@ struct Tuning {
     int psrt = 0, psbv = 0, pscpw = 0, psrb = 0;  // PSRT, PSBV, PSCPW, PSRB: its variant
     int gather = -1;             // GATHER: 0 never the direct-gather kernel, 1 wherever it runs
     int gct = 0, gnw = 0, gd = 0;  // GCT, GNW, GD: its variant
+    int gh = 0;                  // GH: 1 one workgroup per strip, 2 row halves of 64 rows (above 64 rows)
     int rg = -1;                 // RG: 0 never the row-gather kernel, 1 wherever it runs
     int rgct = 0, rgnw = 0, rgd = 0;  // RGCT, RGNW, RGD: its variant
     const char *tile_or_null() const { return tile[0] ? tile : nullptr; }
@@ -354,7 +356,7 @@ bool parse_tuning(const char *spec, Tuning &t)
                 {"RT", &t.rt}, {"PS", &t.ps}, {"PSRT", &t.psrt}, {"PSBV", &t.psbv},
                 {"PSCPW", &t.pscpw}, {"PSRB", &t.psrb}, {"GATHER", &t.gather}, {"GCT", &t.gct},
                 {"GNW", &t.gnw}, {"GD", &t.gd}, {"RG", &t.rg}, {"RGCT", &t.rgct}, {"RGNW", &t.rgnw},
-                {"RGD", &t.rgd}};
+                {"RGD", &t.rgd}, {"GH", &t.gh}};
             bool found = false;
             for (const auto &f : fields)
                 if (std::strcmp(key, f.name) == 0) { *f.field = (int)v; found = true; }
@@ -782,12 +784,36 @@ bool plan_gather(const float *Bc, int64_t m, int64_t n, int64_t k, int N, int M,
         splits = std::max<int64_t>(1, std::min<int64_t>((256 + strips - 1) / strips, nquads / (8 * c.NW)));
     const int fs = t.splits;
     if (fs >= 1) splits = std::min<int64_t>(fs, std::max<int64_t>(nquads, 1));
-    if (strips * splits > INT32_MAX) return false;
+    // Above 64 rows without split-k, on short strips: two row halves of 64
+    // rows, each a workgroup of the 64-row variant (two per CU; the halves of
+    // a strip share its Bc lines through one XCD's L2), where the 128-row
+    // variant has one wave per SIMD and few trips of its ring.  Measured
+    // (graph replay, m x k x n): at w <= 512 compressed rows on 256 strips
+    // 128 x 1024 x 8192 at 4:32 12.8 -> 11.2 us, 128 x 2048 x 8192 15.5 ->
+    // 13.8, 80 x 2048 x 8192 14.7 -> 13.4, 72 x 3072 x 8192 17.3 -> 16.0,
+    // 128 x 4096 x 8192 20.7 -> 19.3, 128 x 2048 x 8192 at 8:32 19.9 -> 18.2;
+    // slower at w = 1024 (128 x 8192 x 8192 at 4:32 29.5 -> 30.8) and where
+    // the doubled grid no longer fits two workgroups per CU (128 x 4096 x
+    // 16384 at 4:32 29.6 -> 31.7).
+    // (A forced variant, GCT / GNW / GD, keeps one workgroup per strip unless
+    // GH = 2 asks for the halves.)
+    const bool halves = t.gh == 2 || (t.gh == 0 && !t.gct && !t.gnw && !t.gd && w <= 512 && strips <= 256);
+    if (halves && m > 64 && splits == 1) {
+        GatherCfg h = c;
+        h.RT = 4;
+        h.H = 2;
+        h.CT = t.gct ? t.gct : defaults[4][0];
+        h.NW = t.gnw ? t.gnw : defaults[4][1];
+        h.D = t.gd ? t.gd : defaults[4][2];
+        if (gather_has(h) && V % (16 * h.CT) == 0 && n / (16 * h.CT) == strips) c = h;
+    }
+    if (strips * splits * c.H > INT32_MAX) return false;
     p.kind = Kind::Gather;
     p.RT = c.RT;
     p.CT = c.CT;
     p.NW = c.NW;
     p.D = c.D;
+    p.H = c.H;
     p.splits = (int)splits;
     p.tiles_m = 1;
     p.tiles_n = (int)strips;
@@ -881,7 +907,10 @@ hipError_t launch_main(const Plan &p, const float *A, const float *Bc, const uin
         g.splits = p.splits;
         g.epi = epi;
         g.ws = ws;
-        return launch_gather(GatherCfg{p.RT, p.CT, p.NW, p.D}, g, stream);
+        g.halves = p.H;
+        GatherCfg gc{p.RT, p.CT, p.NW, p.D};
+        gc.H = p.H;
+        return launch_gather(gc, g, stream);
     }
     if (p.kind == Kind::RowGather) {
         RowGatherArgs g;
@@ -992,6 +1021,11 @@ const char *plan_name(const Plan &p, bool with_ws)
     thread_local char buf[160];
     if (p.kind == Kind::RowGather) {
         std::snprintf(buf, sizeof buf, "nm_rowgather_kernel<r%d,c%d,w%d,d%d>,split1", 16 * p.RT, p.COLS, p.NW, p.D);
+        return buf;
+    }
+    if (p.kind == Kind::Gather && p.H > 1) {
+        std::snprintf(buf, sizeof buf, "nm_gather_kernel<r%dx%d,c%d,w%d,d%d>+prep,split%d", gather_rows(p.RT), p.H,
+                      p.COLS, p.NW, p.D, p.splits);
         return buf;
     }
     if (p.kind == Kind::Gather) {

@@ -354,6 +354,12 @@ def test_dispatch_rules_for_short_products():
     ws = nm.nmspmm_kernel_name_ws
     assert ws(64, 8192, 8192, 4, 32, 64).startswith("nm_gather_kernel<")                    # 256 strips
     assert ws(40, 8192, 1536, 4, 32, 64).startswith("nm_gather_kernel<r64,")
+    # above 64 rows on short strips (w <= 512, 256 strips): two row halves of 64
+    assert ws(128, 8192, 2048, 4, 32, 64) == "nm_gather_kernel<r64x2,c32,w8,d4>+prep,split1"
+    assert ws(80, 8192, 2048, 4, 32, 64) == "nm_gather_kernel<r64x2,c32,w8,d4>+prep,split1"
+    assert ws(128, 8192, 8192, 4, 32, 64) == "nm_gather_kernel<r128,c32,w4,d4>+prep,split1"     # w = 1024
+    assert ws(128, 16384, 4096, 4, 32, 64) == "nm_gather_kernel<r128,c32,w4,d4>+prep,split1"    # 512 strips
+    assert ws(128, 8192, 2048, 4, 32, 64, tuning={"GH": 1}) == "nm_gather_kernel<r128,c32,w4,d4>+prep,split1"
     assert ws(128, 4096, 4096, 4, 32, 64).startswith("nm_stream_kernel<")                   # 128 strips
     assert ws(128, 512, 512, 16, 32, 32).startswith("nm_skinny_kernel<c32,")
     assert nm.nmspmm_workspace_bytes(128, 512, 512, 16, 32, 32) == 0

@@ -767,7 +767,9 @@ def test_gather_kernel_exact(shape, splits):
     m, k, n, N, M, V = shape
     name = kname_ws(m, n, k, N, M, V)
     say(f"[gather] {shape} {name}")
-    assert name.startswith("nm_gather_kernel<r%d," % (16 if m <= 16 else 32 if m <= 32 else 64 if m <= 64 else 128))
+    rows = 16 if m <= 16 else 32 if m <= 32 else 64 if m <= 64 else 128
+    # above 64 rows without split-k on short strips: two row halves of 64
+    assert name.startswith(("nm_gather_kernel<r%d," % rows,) + (("nm_gather_kernel<r64x2,",) if m > 64 else ()))
     w = k // M * N
     if splits != "auto" and (w + 3) // 4 >= 3:
         assert name.endswith(",split3")
@@ -821,6 +823,36 @@ def test_gather_variants_exact(variant, splits):
     C = run_ws(A, Bc, idx, m, n, k, N, M, V, ws)
     assert bool(np.array_equal(C.astype(np.float64), oracle.spmm(A, Bc, idx, m, n, k, N, M, V)))
     A, Bp, _ = make_inputs(m, k, n, N, M, V, 37 + m, "normal")
+    Bc, idx = oracle.compress(Bp, N, M, V)
+    C = run_ws(A, Bc, idx, m, n, k, N, M, V, ws)
+    r = oracle.check(C, oracle.spmm(A, Bc, idx, m, n, k, N, M, V), oracle.bound(A, Bc, idx, m, n, k, N, M, V))
+    assert r, (name, r)
+
+
+@pytest.mark.parametrize("shape", [(65, 1024, 512, 4, 32, 64), (100, 832, 768, 1, 8, 128), (128, 2048, 1024, 16, 32, 32),
+                                   (97, 776, 320, 3, 8, 32)], ids=lambda s: "x".join(map(str, s)))
+def test_gather_row_halves_exact(shape):
+    """Above 64 rows, the direct-gather kernel forced into two row halves of
+    64 rows (each half its own workgroup and At; the second half ragged):
+    bit-exact on small integers twice in a row on one workspace, the epilogue
+    applied once, normal data within the bar."""
+    TUNE.update({"GATHER": "1", "SPLITS": "1", "GH": "2"})
+    m, k, n, N, M, V = shape
+    name = kname_ws(m, n, k, N, M, V)
+    say(f"[gather halves] {shape} {name}")
+    assert name.startswith("nm_gather_kernel<r64x2,")
+    ws = new_workspace(m, n, k, N, M, V)
+    A, Bp, _ = make_inputs(m, k, n, N, M, V, 17 + m, "int")
+    Bc, idx = oracle.compress(Bp, N, M, V)
+    C_ref = oracle.spmm(A, Bc, idx, m, n, k, N, M, V)
+    for _ in range(2):
+        C = run_ws(A, Bc, idx, m, n, k, N, M, V, ws)
+        assert bool(np.array_equal(C.astype(np.float64), C_ref)), \
+            f"{int(np.count_nonzero(C.astype(np.float64) != C_ref))} outputs differ"
+    bias = np.random.default_rng(n).integers(-50, 50, n).astype(np.float32)
+    Y = run_ws(A, Bc, idx, m, n, k, N, M, V, ws, alpha=4.0, bias=bias, act="relu")
+    assert bool(np.array_equal(Y.astype(np.float64), oracle.epilogue(C_ref, 4.0, bias, "relu")))
+    A, Bp, _ = make_inputs(m, k, n, N, M, V, 19 + m, "normal")
     Bc, idx = oracle.compress(Bp, N, M, V)
     C = run_ws(A, Bc, idx, m, n, k, N, M, V, ws)
     r = oracle.check(C, oracle.spmm(A, Bc, idx, m, n, k, N, M, V), oracle.bound(A, Bc, idx, m, n, k, N, M, V))
