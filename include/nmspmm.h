@@ -274,6 +274,8 @@ NMSPMM_API nmspmm_status_t nmspmm_run_noalloc(const float *A, const float *Bc, c
  *                              per wave and ring rows
  *   GATHER  0: never the direct-gather kernel, 1: wherever it runs
  *   GCT, GNW, GD               its column tiles, waves and ring depth
+ *   GH      1: one direct-gather workgroup per strip, 2: two row halves of
+ *           64 rows each (above 64 rows, without split-k)
  *   RG      0: never the row-gather kernel, 1: wherever it runs (up to 32
  *           rows, V a multiple of 32)
  *   RGCT, RGNW, RGD            its column tiles, waves and ring depth
