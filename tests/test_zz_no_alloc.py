@@ -23,12 +23,14 @@ import paper_2503_01253_amd as nm  # noqa: E402
 # (transposed A and offsets in the scratch), the pipelined streaming kernel
 # with split-k partial tiles in the scratch (V = 16 keeps the gather kernel
 # out), the direct-gather kernel at 40 rows, and the register-operand
-# streaming kernel, which takes no scratch at all.
+# streaming kernel, which takes no scratch at all; then the direct-gather
+# kernel in two row halves of 64 rows (128 rows on short strips).
 CASES = [
     (128, 8192, 8192, 4, 32, 64),
     (64, 4096, 2048, 4, 32, 16),
     (40, 1536, 8192, 4, 32, 64),
     (16, 2048, 1024, 4, 32, 64),
+    (128, 2048, 8192, 4, 32, 64),
 ]
 
 
@@ -68,6 +70,7 @@ def test_noalloc_matches_run_ws_on_consecutive_calls():
         assert r, (name, r)
     assert names[0].startswith("nm_gather_kernel<r128,") and "+ws,split" in names[1]
     assert names[2].startswith("nm_gather_kernel<r64,") and names[3].startswith("nm_skinny_kernel")
+    assert names[4].startswith("nm_gather_kernel<r64x2,")
 
 
 def test_noalloc_epilogue_matches_run_ws():
