@@ -19,9 +19,10 @@
  *
  * Every entry point is extern "C", returns a status code and never throws.
  * The library's only global state is the static scratch array of
- * nmspmm_run_noalloc (with its per-device address) and one memory pool per
- * device for the workspaces of nmspmm_run and nmspmm_run_ex, created on
- * first use; it is safe to call from several host threads.
+ * nmspmm_run_noalloc (with its per-device address) and a table of at most 16
+ * cached workspaces of nmspmm_run and nmspmm_run_ex, one per (device,
+ * stream), allocated on first use and kept until the process ends; it is
+ * safe to call from several host threads.
  */
 #ifndef NMSPMM_H
 #define NMSPMM_H
@@ -94,12 +95,14 @@ NMSPMM_API nmspmm_status_t nmspmm_compress(const float *B_dense, int64_t k, int6
  * synchronize.  Kernel faults surface at the caller's next synchronization.
  * Workspace: where nmspmm_run_ws would run the direct-gather kernel (the
  * "+prep" names of nmspmm_kernel_name_ws), the call takes that kernel's
- * workspace from a memory pool the library owns on the current device,
- * allocated and released on `stream` around its kernels
- * (hipMallocFromPoolAsync / hipFreeAsync; the pool keeps up to 256 MiB
- * between calls), and the result is bit-identical to nmspmm_run_ws's.
- * While `stream` is being captured into a graph, or when the pool cannot
- * provide the memory, it runs the kernels that take none instead (named by
+ * workspace from a buffer the library keeps for `stream` on the current
+ * device (hipMalloc on the first call that needs it, and again, larger, on
+ * a call that needs more; the call's kernels are ordered after the buffer's
+ * previous use by an event), and the result is bit-identical to
+ * nmspmm_run_ws's.  Up to 16 such buffers are kept; a call on a further
+ * stream releases the least recently used idle one.  While `stream` is
+ * being captured into a graph, or when no buffer can be had, it runs the
+ * kernels that take none instead (named by
  * nmspmm_kernel_name_tuned with with_workspace = 0), as it does for every
  * other shape.  Callers that cannot allocate at all use nmspmm_run_noalloc.  m == 0 or n == 0 returns NMSPMM_OK without a launch;
  * k == 0 writes zeros to C.  Summation order: fp32 MFMA accumulation in an
@@ -166,8 +169,8 @@ NMSPMM_API int64_t nmspmm_workspace_bytes(int64_t m, int64_t n, int64_t k, int N
  *              Either way: no zero fill of C, no atomics, and the result
  *              does not vary between runs.  Otherwise (NULL, smaller, or a
  *              shape whose kernel takes none) the call runs exactly as
- *              nmspmm_run_ex (which takes a pooled workspace where the
- *              shape's kernel is the direct-gather kernel).
+ *              nmspmm_run_ex (which takes its cached workspace where
+ *              the shape's kernel is the direct-gather kernel).
  * A workspace serves one call at a time: calls that overlap on one workspace
  * (on different streams) race.  Arguments, asynchrony and errors otherwise
  * as nmspmm_run_ex, plus NMSPMM_ERR_UNSUPPORTED for a workspace not aligned
@@ -223,7 +226,7 @@ NMSPMM_API nmspmm_status_t nmspmm_validate_idx(const uint8_t *idx, int64_t k, in
 NMSPMM_API const char *nmspmm_status_string(nmspmm_status_t s);
 
 /* Name of the kernel variant nmspmm_run would launch for this shape outside
- * graph capture (the direct-gather kernel with its pooled workspace where
+ * graph capture (the direct-gather kernel with its cached workspace where
  * nmspmm_kernel_name_ws names it), assuming buffers aligned as the
  * allocator returns them: "none" when nothing is
  * launched, "invalid" for a bad shape.  The string stays valid until the next
@@ -285,7 +288,7 @@ NMSPMM_API nmspmm_status_t nmspmm_run_noalloc(const float *A, const float *Bc, c
  * NMSPMM_ERR_INVALID_ARG ("invalid" / -1 for the two queries).  Arguments,
  * layout, asynchrony, workspace rules and errors otherwise as
  * nmspmm_run_ws, except that without a large enough workspace the call runs
- * the kernels that take none (it takes no pooled workspace). */
+ * the kernels that take none (it takes no cached workspace). */
 NMSPMM_API nmspmm_status_t nmspmm_run_tuned(const float *A, const float *Bc, const uint8_t *idx,
                                  float *C, int64_t m, int64_t n, int64_t k, int N,
                                  int M, int V, float alpha, const float *bias,
@@ -293,7 +296,7 @@ NMSPMM_API nmspmm_status_t nmspmm_run_tuned(const float *A, const float *Bc, con
                                  const char *tuning, hipStream_t stream);
 
 /* Under the overrides of `tuning`: the kernels nmspmm_run_tuned launches
- * without a workspace (with_workspace == 0; the tuned call takes no pooled
+ * without a workspace (with_workspace == 0; the tuned call takes no cached
  * workspace) or with one of nmspmm_workspace_bytes_tuned bytes (otherwise,
  * as nmspmm_kernel_name_ws). */
 NMSPMM_API const char *nmspmm_kernel_name_tuned(int64_t m, int64_t n, int64_t k, int N, int M, int V,

@@ -1078,7 +1078,7 @@ extern "C" const char *nmspmm_kernel_name_tuned(int64_t m, int64_t n, int64_t k,
 
 extern "C" const char *nmspmm_kernel_name(int64_t m, int64_t n, int64_t k, int N, int M, int V)
 {
-    // outside graph capture nmspmm_run takes the workspace plan, with a pooled
+    // outside graph capture nmspmm_run takes the workspace plan, with the stream's cached
     // workspace, where that plan is the direct-gather kernel
     const char *with_ws = nmspmm_kernel_name_tuned(m, n, k, N, M, V, 1, nullptr);
     if (std::strncmp(with_ws, "nm_gather_kernel<", 17) == 0) return with_ws;
@@ -1111,49 +1111,113 @@ nmspmm_status_t check_run_args(const float *A, const float *Bc, const uint8_t *i
 }
 
 // Workspaces of the calls that bring none (nmspmm_run, nmspmm_run_ex): one
-// memory pool per device, owned by the library and created on its first use
-// there.  A call allocates from it and releases to it on its own stream
-// (stream-ordered: the next call on any stream reuses the memory only after
-// this call's kernels), and the pool keeps up to kPoolKeep bytes between
-// calls, so that a steady stream of calls maps no new memory.
-constexpr int kPoolDevices = 64;
-constexpr uint64_t kPoolKeep = uint64_t(256) << 20;
-std::atomic<hipMemPool_t> g_pool[kPoolDevices];
-std::mutex g_pool_mu;
+// buffer per (device, stream), allocated on the first call that needs it
+// (and again, larger, when a call needs more) and kept for the next calls on
+// that stream.  Each call makes its stream wait for the event the buffer's
+// previous user recorded after its kernels, and records it again after its
+// own.  Calls on one stream are ordered anyway; the wait orders the first
+// call on a stream whose handle reuses that of a destroyed one (HIP hands a
+// new stream the last destroyed stream's handle) after the destroyed
+// stream's last kernels.  The pair costs about 1.4 us of host time per call
+// and no measurable GPU time (MI355X), where a stream-ordered allocation
+// from a memory pool and its release cost 8.7 us and made back-to-back calls
+// host-bound.  At
+// most kWsEntries buffers are kept: a call past that releases the oldest
+// idle entry's buffer once that entry's last kernels are done (an entry a
+// call is between acquiring and marking is never released or regrown; a call
+// that finds none it may use runs without a workspace).
+constexpr int kWsEntries = 16;
+struct WsEntry {
+    int dev = -1;
+    hipStream_t stream = nullptr;
+    void *buf = nullptr;
+    size_t bytes = 0;
+    hipEvent_t done = nullptr;
+    uint64_t used = 0;   // call counter of the last use (for the oldest entry)
+    int busy = 0;        // calls between ws_acquire and ws_done (never dropped then)
+};
+WsEntry g_ws[kWsEntries];
+uint64_t g_ws_calls = 0;
+std::mutex g_ws_mu;
 
-hipError_t pool_on_current_device(hipMemPool_t *out)
+// Release an entry's buffer and event after its last kernels.
+void ws_drop(WsEntry &e)
+{
+    if (e.done) (void)hipEventSynchronize(e.done);
+    if (e.buf) (void)hipFree(e.buf);
+    if (e.done) (void)hipEventDestroy(e.done);
+    e = WsEntry{};
+}
+
+// A workspace of at least `need` bytes for a call on `stream` (the current
+// device), ordered after the buffer's previous use; null when none can be
+// had.  ws_done(...) must follow the call's launches.
+void *ws_acquire(hipStream_t stream, size_t need, int *slot)
 {
     int dev = -1;
-    hipError_t e = hipGetDevice(&dev);
-    if (e != hipSuccess) return e;
-    if (dev < 0 || dev >= kPoolDevices) return hipErrorInvalidDevice;
-    hipMemPool_t pool = g_pool[dev].load(std::memory_order_acquire);
-    if (!pool) {
-        std::lock_guard<std::mutex> lock(g_pool_mu);
-        pool = g_pool[dev].load(std::memory_order_relaxed);
-        if (!pool) {
-            hipMemPoolProps props = {};
-            props.allocType = hipMemAllocationTypePinned;
-            props.handleTypes = hipMemHandleTypeNone;
-            props.location.type = hipMemLocationTypeDevice;
-            props.location.id = dev;
-            e = hipMemPoolCreate(&pool, &props);
-            if (e != hipSuccess) return e;
-            uint64_t keep = kPoolKeep;
-            e = hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &keep);
-            if (e != hipSuccess) {
-                (void)hipMemPoolDestroy(pool);
-                return e;
-            }
-            g_pool[dev].store(pool, std::memory_order_release);
+    if (hipGetDevice(&dev) != hipSuccess) {
+        (void)hipGetLastError();
+        return nullptr;
+    }
+    std::lock_guard<std::mutex> lock(g_ws_mu);
+    int hit = -1, oldest = -1;
+    for (int i = 0; i < kWsEntries; ++i) {
+        if (g_ws[i].buf && g_ws[i].dev == dev && g_ws[i].stream == stream) hit = i;
+        if (g_ws[i].buf && g_ws[i].busy == 0 && (oldest < 0 || g_ws[i].used < g_ws[oldest].used)) oldest = i;
+    }
+    int i = hit;
+    if (i >= 0 && g_ws[i].bytes < need) {
+        if (g_ws[i].busy > 0) return nullptr;
+        ws_drop(g_ws[i]);   // grow: the old buffer after its last use
+    }
+    if (i < 0) {
+        for (int j = 0; j < kWsEntries && i < 0; ++j)
+            if (!g_ws[j].buf) i = j;
+        if (i < 0) {
+            if (oldest < 0) return nullptr;
+            i = oldest;
+            ws_drop(g_ws[i]);
         }
     }
-    *out = pool;
-    return hipSuccess;
+    WsEntry &e = g_ws[i];
+    if (!e.buf) {
+        const size_t bytes = (need + 255) / 256 * 256;
+        if (hipMalloc(&e.buf, bytes) != hipSuccess) {
+            e = WsEntry{};
+            (void)hipGetLastError();
+            return nullptr;
+        }
+        // completion order only: the next user overwrites the buffer before
+        // reading it, so no system-scope fence (cache write-back) is needed
+        if (hipEventCreateWithFlags(&e.done, hipEventDisableTiming | hipEventDisableSystemFence) != hipSuccess) {
+            (void)hipFree(e.buf);
+            e = WsEntry{};
+            (void)hipGetLastError();
+            return nullptr;
+        }
+        e.dev = dev;
+        e.stream = stream;
+        e.bytes = bytes;
+    } else if (hipStreamWaitEvent(stream, e.done, 0) != hipSuccess) {
+        (void)hipGetLastError();
+        return nullptr;
+    }
+    e.used = ++g_ws_calls;
+    ++e.busy;
+    *slot = i;
+    return e.buf;
+}
+
+// After the call's launches on `stream`: mark the buffer's last use.
+hipError_t ws_done(int slot, hipStream_t stream)
+{
+    std::lock_guard<std::mutex> lock(g_ws_mu);
+    --g_ws[slot].busy;
+    return hipEventRecord(g_ws[slot].done, stream);
 }
 
 // Whether work on `stream` is being captured into a graph (or that cannot be
-// told): such calls take no pooled workspace.
+// told): such calls take no cached workspace.
 bool capturing(hipStream_t stream)
 {
     hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
@@ -1165,14 +1229,14 @@ bool capturing(hipStream_t stream)
 }
 
 // `pooled`: a call whose workspace (if any) is smaller than its workspace
-// plan needs takes one from the pool instead, outside graph capture, where
-// that plan is the direct-gather kernel; when the pool cannot give one, the
-// call runs the plan that takes none.  The pool's allocation and release
-// cost about 5 us per call (MI355X, eager launches): the direct-gather
-// kernel gains more (64 x 8192 x 8192 at 4:32 30.2 -> 26.2 us, 128 rows
-// 42.3 -> 36.2), the streaming kernels' split-k through a workspace does not
-// (64 x 2048 x 4096 at 4:32, V = 16: 16.3 -> 21.0 us), and keeps its atomics
-// there.
+// plan needs takes the stream's cached workspace instead, outside graph
+// capture, where that plan is the direct-gather kernel; when none can be
+// had, the call runs the plan that takes none.  (Measured on MI355X, 2000
+// back-to-back calls from C++ at 64 x 8192 x 8192, 4:32: caller workspace
+// 15.5 us per call, the cached workspace 18.2, no workspace (split-k,
+// atomics) 25.4; at 128 rows 26.4, 28.8 and 37.5.  The streaming kernels'
+// split-k through a workspace gains less than the workspace costs and keeps
+// its atomics there.)
 nmspmm_status_t run_impl(const float *A, const float *Bc, const uint8_t *idx, float *C, int64_t m, int64_t n,
                          int64_t k, int N, int M, int V, float alpha, const float *bias, nmspmm_act_t act,
                          void *workspace, size_t ws_bytes, const Tuning &t, hipStream_t stream,
@@ -1181,24 +1245,17 @@ nmspmm_status_t run_impl(const float *A, const float *Bc, const uint8_t *idx, fl
     const nmspmm_status_t st = check_run_args(A, Bc, idx, C, m, n, k, N, M, V, bias, act);
     if (st != NMSPMM_OK || m == 0 || n == 0) return st;
     if (workspace && !aligned(workspace, 256)) return NMSPMM_ERR_UNSUPPORTED;
-    void *from_pool = nullptr;
+    int cached = -1;
     if (pooled) {
         const Plan pw = make_ws_plan(A, Bc, C, m, n, k, N, M, V, t);
         const int64_t need = pw.kind == Kind::Gather ? plan_ws_bytes(pw) : 0;
         if (need > 0 && (!workspace || (uint64_t)need > (uint64_t)ws_bytes) && !capturing(stream)) {
-            // a failed call here leaves its error behind: clear it, so that
-            // the launches' own error checks do not report it
-            hipMemPool_t pool = nullptr;
-            if (pool_on_current_device(&pool) != hipSuccess ||
-                hipMallocFromPoolAsync(&from_pool, (size_t)need, pool, stream) != hipSuccess) {
-                from_pool = nullptr;
-                (void)hipGetLastError();
-            } else if (!aligned(from_pool, 256)) {
-                (void)hipFreeAsync(from_pool, stream);
-                from_pool = nullptr;
-            } else {
-                workspace = from_pool;
+            void *buf = ws_acquire(stream, (size_t)need, &cached);
+            if (buf) {
+                workspace = buf;
                 ws_bytes = (size_t)need;
+            } else {
+                cached = -1;
             }
         }
     }
@@ -1207,7 +1264,7 @@ nmspmm_status_t run_impl(const float *A, const float *Bc, const uint8_t *idx, fl
     Plan p = workspace ? make_ws_plan(A, Bc, C, m, n, k, N, M, V, t) : make_plan(A, Bc, C, m, n, k, N, M, V, t);
     if (workspace && (uint64_t)plan_ws_bytes(p) > (uint64_t)ws_bytes) p = make_plan(A, Bc, C, m, n, k, N, M, V, t);
     if (p.kind == Kind::None) {
-        if (from_pool) (void)hipFreeAsync(from_pool, stream);
+        if (cached >= 0) (void)ws_done(cached, stream);
         return NMSPMM_OK;
     }
     Epilogue epi;
@@ -1217,7 +1274,7 @@ nmspmm_status_t run_impl(const float *A, const float *Bc, const uint8_t *idx, fl
     const int64_t need = plan_ws_bytes(p);
     void *ws = need > 0 && workspace && (uint64_t)need <= (uint64_t)ws_bytes ? workspace : nullptr;
     const hipError_t e = launch_plan(p, A, Bc, idx, C, m, n, k, N, M, V, epi, ws, stream);
-    const hipError_t f = from_pool ? hipFreeAsync(from_pool, stream) : hipSuccess;
+    const hipError_t f = cached >= 0 ? ws_done(cached, stream) : hipSuccess;
     return e == hipSuccess && f == hipSuccess ? NMSPMM_OK : NMSPMM_ERR_HIP;
 }
 

@@ -311,7 +311,7 @@ def test_confusion_argument_checks_without_a_launch():
 
 def test_run_names_its_workspace_plan():
     """nmspmm_kernel_name names what nmspmm_run launches outside graph
-    capture: the direct-gather kernel with a pooled workspace where
+    capture: the direct-gather kernel with its cached workspace where
     nmspmm_kernel_name_ws names it, the kernels that take no workspace
     everywhere else (the tuned query without a workspace)."""
     L = nm.lib()

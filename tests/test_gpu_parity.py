@@ -4,6 +4,8 @@ Bar: every element finite and |C_gpu - C_ref| <= 1e-5 * sum_k |A_ik||B_kj|
 (fp32 arithmetic against an fp64 reference), and bit-exact equality on
 small-integer inputs whose partial sums are all exact in fp32.
 """
+import ctypes
+import os
 import sys
 
 import numpy as np
@@ -638,24 +640,24 @@ def test_run_ws_graph_replay(gather):
         assert bool(np.array_equal(dC.cpu().numpy().view(np.uint32), eager.view(np.uint32))), f"replay {i}"
 
 
-# ---- pooled workspaces of nmspmm_run / nmspmm_run_ex ----
-POOLED_SHAPES = [
+# ---- cached workspaces of nmspmm_run / nmspmm_run_ex ----
+CACHED_WS_SHAPES = [
     (64, 8192, 8192, 4, 32, 64),    # R5b
     (128, 2048, 8192, 4, 32, 64),   # 128 rows
     (40, 1536, 8192, 4, 32, 64),    # 40 rows in the 64-row variant
 ]
 
 
-@pytest.mark.parametrize("shape", POOLED_SHAPES, ids=lambda s: "x".join(map(str, s)))
-def test_run_takes_pooled_workspace(shape):
+@pytest.mark.parametrize("shape", CACHED_WS_SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_run_takes_cached_workspace(shape):
     """Outside graph capture nmspmm_run and nmspmm_run_ex take the direct-
-    gather kernel with a workspace from the library's pool where
+    gather kernel with the workspace the library keeps for the stream where
     nmspmm_run_ws would run it: the name is that of nmspmm_kernel_name_ws, and
     the output is bit-identical to nmspmm_run_ws's (with and without the
     epilogue), twice in a row, and within the bar."""
     m, k, n, N, M, V = shape
     name = nm.nmspmm_kernel_name(m, n, k, N, M, V)
-    say(f"[pooled] {shape} {name}")
+    say(f"[cached ws] {shape} {name}")
     assert name == nm.nmspmm_kernel_name_ws(m, n, k, N, M, V)
     assert name.startswith("nm_gather_kernel<")
     A, Bp, _ = make_inputs(m, k, n, N, M, V, 51 + m, "normal")
@@ -715,8 +717,8 @@ def test_run_under_capture_takes_no_workspace():
         assert oracle.check(eager.cpu().numpy(), C_ref, Bnd)
 
 
-def test_run_pooled_workspaces_on_two_streams():
-    """Calls on two streams at once each take their own pooled workspace: both
+def test_run_cached_workspaces_on_two_streams():
+    """Calls on two streams at once each take their own cached workspace: both
     outputs bit-identical to nmspmm_run_ws's."""
     m, k, n, N, M, V = 64, 8192, 8192, 4, 32, 64
     A, Bp, _ = make_inputs(m, k, n, N, M, V, 71, "normal")
@@ -737,6 +739,43 @@ def test_run_pooled_workspaces_on_two_streams():
         torch.cuda.synchronize()
         for o, r in zip(outs, ref):
             assert torch.equal(o.view(torch.int32), r.view(torch.int32))
+
+
+def test_run_cached_workspace_on_a_reused_stream_handle():
+    """HIP hands a new stream the handle of the stream destroyed just before;
+    the workspace cached for that handle is then ordered after the destroyed
+    stream's last kernels, which are still running when the new stream's
+    call is enqueued.  Both outputs bit-identical to nmspmm_run_ws's."""
+    hip = ctypes.CDLL(os.path.join(os.path.dirname(torch.__file__), "lib", "libamdhip64.so"))
+    m, k, n, N, M, V = 128, 2048, 8192, 4, 32, 64
+    assert nm.nmspmm_kernel_name(m, n, k, N, M, V).startswith("nm_gather_kernel<")
+    A, Bp, _ = make_inputs(m, k, n, N, M, V, 73, "normal")
+    Bc, idx = oracle.compress(Bp, N, M, V)
+    dA, dBc, didx = to_dev(A), to_dev(Bc), to_dev(idx)
+    A2 = torch.randn((m, k), device="cuda")
+    ref = [torch.empty((m, n), device="cuda") for _ in range(2)]
+    ws = new_workspace(m, n, k, N, M, V)
+    for a, r in zip((dA, A2), ref):
+        nm.nmspmm_run_ws(a, dBc, didx, r, m, n, k, N, M, V, ws)
+    torch.cuda.synchronize()
+    reused = 0
+    for _ in range(3):
+        outs = [torch.full((m, n), float("nan"), device="cuda") for _ in range(2)]
+        torch.cuda.synchronize()
+        handles = []
+        for a, o in zip((dA, A2), outs):
+            h = ctypes.c_void_p()
+            assert hip.hipStreamCreate(ctypes.byref(h)) == 0
+            handles.append(h.value)
+            st = torch.cuda.ExternalStream(h.value)
+            for _ in range(4):   # a queue of work still running at the destroy
+                nm.nmspmm_run(a, dBc, didx, o, m, n, k, N, M, V, stream=st)
+            assert hip.hipStreamDestroy(h) == 0
+        reused += handles[0] == handles[1]
+        torch.cuda.synchronize()
+        for o, r in zip(outs, ref):
+            assert torch.equal(o.view(torch.int32), r.view(torch.int32))
+    say(f"[cached ws] reused stream handles: {reused} of 3")
 
 
 # ---- direct-gather kernel (nmspmm_run_ws on short products) ----
