@@ -430,7 +430,61 @@ def measure_extras(torch, nm):
                     "alg_gb_s": round(gbs, 1), "frac_hbm_peak": round(gbs / PEAK_HBM_GBS, 3)})
         torch.cuda.empty_cache()
     out["decode_batches"] = {"workload": "m x 8192 x 8192 (m x n x k), 4:32, V=64, normal seed=1008", "runs": dec}
+    out["plain_call"] = plain_call(torch, nm)
     return out
+
+
+def time_batch(torch, fn, steps, warmup):
+    """Whole-batch time per call of `steps` back-to-back launches (events
+    around the batch only, so nothing is enqueued between the calls)."""
+    warm_gpu(torch, fn, 0.2)
+    for i in range(warmup):
+        fn(i)
+    torch.cuda.synchronize()
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for i in range(steps):
+        fn(warmup + i)
+    t1.record()
+    torch.cuda.synchronize()
+    return t0.elapsed_time(t1) / steps
+
+
+def plain_call(torch, nm):
+    """nmspmm_run as a caller without a workspace makes it on the short
+    products (the direct-gather kernel with the workspace the library caches
+    for the stream), against nmspmm_run_ws with a caller workspace and against
+    the kernels that take none: eager launches from Python, back to back."""
+    L = nm.lib()
+    h = torch.cuda.current_stream().cuda_stream
+    rows = []
+    for name in ("R5b", "R5c"):
+        r = RUNS[name]
+        w = Workload(r, torch, nm, min_copies=2)
+
+        def plain(i, w=w, r=r):
+            a, b, x, c = w.ptrs[i % w.copies]
+            if L.nmspmm_run(a, b, x, c, r.m, r.n, r.k, r.N, r.M, r.V, h) != 0:
+                raise RuntimeError("nmspmm_run failed")
+
+        def none(i, w=w, r=r):
+            a, b, x, c = w.ptrs[i % w.copies]
+            if L.nmspmm_run_tuned(a, b, x, c, r.m, r.n, r.k, r.N, r.M, r.V, ctypes.c_float(1.0), None, 0,
+                                  None, 0, None, h) != 0:
+                raise RuntimeError("nmspmm_run_tuned failed")
+
+        us = {lab: round(1e3 * statistics.median(time_batch(torch, fn, 400, 20) for _ in range(3)), 2)
+              for lab, fn in (("nmspmm_run_us", plain), ("nmspmm_run_ws_us", lambda i, w=w: w.launch(i, h)),
+                              ("no_workspace_us", none))}
+        rows.append({"workload": name, "kernel": nm.nmspmm_kernel_name(r.m, r.n, r.k, r.N, r.M, r.V),
+                     "kernel_no_workspace":
+                         L.nmspmm_kernel_name_tuned(r.m, r.n, r.k, r.N, r.M, r.V, 0, None).decode(),
+                     **us})
+        w.free()
+        torch.cuda.empty_cache()
+    return {"timing": "400 back-to-back eager launches from Python, whole-batch time per call, median of 3",
+            "runs": rows}
 
 
 def summary_row(res, roofs):
