@@ -100,7 +100,11 @@ NMSPMM_API nmspmm_status_t nmspmm_compress(const float *B_dense, int64_t k, int6
  * a call that needs more; the call's kernels are ordered after the buffer's
  * previous use by an event), and the result is bit-identical to
  * nmspmm_run_ws's.  Up to 16 such buffers are kept; a call on a further
- * stream releases the least recently used idle one.  While `stream` is
+ * stream releases the least recently used idle one.  Growing or releasing a
+ * buffer waits for its last kernels and calls hipFree, which synchronizes
+ * the device (a graph capture running on another thread in the global
+ * capture mode fails then); callers that mind pass a workspace through
+ * nmspmm_run_ws.  While `stream` is
  * being captured into a graph, or when no buffer can be had, it runs the
  * kernels that take none instead (named by
  * nmspmm_kernel_name_tuned with with_workspace = 0), as it does for every
