@@ -778,6 +778,52 @@ def test_run_cached_workspace_on_a_reused_stream_handle():
     say(f"[cached ws] reused stream handles: {reused} of 3")
 
 
+def test_run_cached_workspaces_past_the_cap_and_from_threads():
+    """More streams than the library keeps buffers for (each new one
+    releases the least recently used idle buffer after its last kernels),
+    then four host threads calling at once on their own streams: every
+    output bit-identical to nmspmm_run_ws's."""
+    import threading
+    m, k, n, N, M, V = 64, 2048, 8192, 4, 32, 64
+    assert nm.nmspmm_kernel_name(m, n, k, N, M, V).startswith("nm_gather_kernel<")
+    A, Bp, _ = make_inputs(m, k, n, N, M, V, 79, "normal")
+    Bc, idx = oracle.compress(Bp, N, M, V)
+    dA, dBc, didx = to_dev(A), to_dev(Bc), to_dev(idx)
+    ref = torch.empty((m, n), device="cuda")
+    nm.nmspmm_run_ws(dA, dBc, didx, ref, m, n, k, N, M, V, new_workspace(m, n, k, N, M, V))
+    torch.cuda.synchronize()
+    streams = [torch.cuda.Stream() for _ in range(20)]
+    outs = [torch.full((m, n), float("nan"), device="cuda") for _ in streams]
+    for st, o in zip(streams, outs):
+        for _ in range(2):
+            nm.nmspmm_run(dA, dBc, didx, o, m, n, k, N, M, V, stream=st)
+    torch.cuda.synchronize()
+    for o in outs:
+        assert torch.equal(o.view(torch.int32), ref.view(torch.int32))
+    errors = []
+
+    def worker(st, o):
+        try:
+            with torch.cuda.stream(st):
+                for _ in range(10):
+                    nm.nmspmm_run(dA, dBc, didx, o, m, n, k, N, M, V, stream=st)
+            st.synchronize()
+        except Exception as e:   # reported by the main thread
+            errors.append(e)
+
+    outs = [torch.full((m, n), float("nan"), device="cuda") for _ in range(4)]
+    torch.cuda.synchronize()
+    threads = [threading.Thread(target=worker, args=(streams[i], outs[i])) for i in range(4)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    assert not errors, errors
+    torch.cuda.synchronize()
+    for o in outs:
+        assert torch.equal(o.view(torch.int32), ref.view(torch.int32))
+
+
 # ---- direct-gather kernel (nmspmm_run_ws on short products) ----
 GATHER_SHAPES = [
     (1, 512, 256, 4, 32, 32),       # one row
