@@ -15,8 +15,9 @@
 // Strip kernel: a workgroup owns all rows (16*RT) x 16*CT columns of C (one
 // strip inside one column block, V a multiple of 16*CT) and, with split-k, a
 // range of quads (4 consecutive compressed rows, the K of
-// v_mfma_f32_16x16x4_f32).  Its NW waves split that range and each streams
-// its quads through a ring of D quads in flight in registers: per quad a
+// v_mfma_f32_16x16x4_f32).  Its NW waves take that range's trips of D quads
+// in turn and each streams its quads through a ring of D quads in flight in
+// registers: per quad a
 // lane loads one offset, RT At floats (one per row tile t, see c_row) and CT
 // consecutive Bc floats (columns CT*(l%16)+s, one per column tile s), and
 // issues RT*CT MFMAs.  No LDS and no barrier in the
@@ -249,15 +250,16 @@ __global__ __launch_bounds__(NW * 64) void nm_gather_kernel(
     const int nquads = (w + 3) / 4;
     const int qs = (int)((int64_t)split * nquads / splits);
     const int qe = (int)((int64_t)(split + 1) * nquads / splits);
-    const int qa = qs + (int)((int64_t)wave * (qe - qs) / NW);
-    const int qb = qs + (int)((int64_t)(wave + 1) * (qe - qs) / NW);
-    const int nq = qb - qa;
+    const int nq = qe - qs;
+    // trips of D quads are dealt to the waves in turn (wave v takes trips v,
+    // v + NW, ...), so that at any time the waves stream one band of Bc
+    const int ntrips = (nq + D - 1) / D;
 
     const int r = lane & 15, kq = lane >> 4;
-    // This wave's Bc rows only: quads past its range (the ring loads one trip
+    // The split's Bc rows only: quads past its range (the ring loads one trip
     // ahead) and rows past w read zero and add nothing.  Offsets past w read
     // zero too, which gathers At row 0, in bounds.
-    const int64_t u_lo = min64(4 * (int64_t)qa, w), u_hi = min64(4 * (int64_t)qb, w);
+    const int64_t u_lo = min64(4 * (int64_t)qs, w), u_hi = min64(4 * (int64_t)qe, w);
     const auto rs_at = make_rsrc(At, (uint32_t)k * ROWS * 4);
     const auto rs_off = make_rsrc(off + (int64_t)b * w + u_lo, (uint32_t)(w - u_lo) * 4);
     const auto rs_bc = make_rsrc(Bc + u_lo * n + j0, (uint32_t)(max64(u_hi - u_lo, 0) * n * 4));
@@ -286,10 +288,10 @@ __global__ __launch_bounds__(NW * 64) void nm_gather_kernel(
     for (int j = 0; j < D; ++j) {
         load_a<RT>(av[j], rs_at, OOB + 1024 * j);   // distinct offsets: no two loads merged
         load_b<CT, BC_AUX>(bv[j], rs_bc, OOB + 64 * j, 0);
-        ov[j] = __builtin_amdgcn_raw_buffer_load_b32(rs_off, (int)lane_off, j * 16, 0);
+        ov[j] = __builtin_amdgcn_raw_buffer_load_b32(rs_off, (int)lane_off, (wave * D + j) * 16, 0);
         __builtin_amdgcn_sched_barrier(0);
     }
-    const int trips = (max(nq, 0) + D - 1) / D;
+    const int trips = ntrips > wave ? (ntrips - wave + NW - 1) / NW : 0;
     // one loop, not peeled: a peeled first trip behind its own branch lets
     // the compiler sink its loads, and the wait counts at the loop head
     // become conservative
@@ -298,11 +300,11 @@ __global__ __launch_bounds__(NW * 64) void nm_gather_kernel(
 #pragma unroll
         for (int j = 0; j < D; ++j) {
             // quads past the wave's range read zero: skip their MFMAs
-            if (t > 0 && (t - 1) * D + j < nq) mma_quad<RT, CT>(acc, av[j], bv[j]);
-            const int qn = t * D + j;
+            if (t > 0 && ((t - 1) * NW + wave) * D + j < nq) mma_quad<RT, CT>(acc, av[j], bv[j]);
+            const int qn = (t * NW + wave) * D + j;
             load_a<RT>(av[j], rs_at, ov[j] + lane_at);
             load_b<CT, BC_AUX>(bv[j], rs_bc, lane_bc, qn * quad_bc);
-            ov[j] = __builtin_amdgcn_raw_buffer_load_b32(rs_off, (int)lane_off, (qn + D) * 16, 0);
+            ov[j] = __builtin_amdgcn_raw_buffer_load_b32(rs_off, (int)lane_off, (qn + NW * D) * 16, 0);
             // keep each slot's loads right after its MFMAs: gathered to the
             // end of the unrolled body, they would be waited for at once
             __builtin_amdgcn_sched_barrier(0);
